@@ -1,0 +1,210 @@
+"""Plain CPU oracle of the ARC-Top-K + EF21M compressor step (ctypes wrapper).
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(``paper_2510_26709_amd`` / libarctopk) never imports it and shares no code
+with it.  Every function here marshals numpy arrays into the C oracle
+(``arc_oracle.c``); the arithmetic, and the citation of the paper passage each
+step follows, live there.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_i32, _i64, _u64, _f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
+_vp = ctypes.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} missing: run __graft_entry__.build() or python oracle/build.py")
+    lib = ctypes.CDLL(_LIB_PATH)
+    sig = {
+        "oracle_splitmix64": (_u64, [_u64, _u64]),
+        "oracle_projection": (ctypes.c_int, [_u64, _i64, _i64, _i32, _vp]),
+        "oracle_momentum": (ctypes.c_int, [_i32, _i64, _f32, _vp, _i32, _vp]),
+        "oracle_sketch": (ctypes.c_int, [_i32, _i64, _i64, _i32, _vp, _vp, _vp, _vp]),
+        "oracle_worker_sum": (ctypes.c_int, [_i32, _i64, _i32, _vp, _vp]),
+        "oracle_importance": (ctypes.c_int, [_i64, _i32, _vp, _vp]),
+        "oracle_select": (ctypes.c_int, [_i64, _vp, _i64, _i32, _vp, _vp, _vp, _vp]),
+        "oracle_gather_update": (ctypes.c_int, [_i32, _i64, _i64, _i64, _vp, _vp, _vp, _vp]),
+        "oracle_step": (ctypes.c_int, [_i32, _i64, _i64, _i32, _f32, _u64, _i64, _i64, _i32,
+                                       _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _vp, _vp]),
+        "oracle_num_threads": (ctypes.c_int, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+class OracleError(ValueError):
+    pass
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise OracleError(f"{what}: invalid argument")
+
+
+def _f32c(a, name):
+    if a.dtype != np.float32 or not a.flags.c_contiguous:
+        raise TypeError(f"{name} must be a C-contiguous float32 array")
+    return a
+
+
+def _grad_args(grad):
+    if grad.dtype == np.float32:
+        return grad, 0
+    if grad.dtype == np.uint16:  # bf16 bit patterns
+        return grad, 1
+    raise TypeError("grad must be float32 or uint16 (bf16 bit patterns)")
+
+
+def num_rows(d: int, n: int) -> int:
+    return -(-d // n)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def splitmix64(seed: int, x: int) -> int:
+    return int(_load().oracle_splitmix64(seed & (2**64 - 1), x & (2**64 - 1)))
+
+
+def projection(seed: int, t: int, n: int, r: int) -> np.ndarray:
+    V = np.empty((n, r), dtype=np.float32)
+    _check(_load().oracle_projection(seed & (2**64 - 1), t, n, r, _ptr(V)), "projection")
+    return V
+
+
+def momentum(h: np.ndarray, grad: np.ndarray, eta: float) -> None:
+    """In place on h ([N, d] float32)."""
+    _f32c(h, "h")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    if grad.shape != h.shape:
+        raise ValueError("grad and h shapes differ")
+    N, d = h.shape
+    _check(_load().oracle_momentum(N, d, eta, _ptr(grad), is_bf16, _ptr(h)), "momentum")
+
+
+def sketch(h: np.ndarray, g: np.ndarray, V: np.ndarray, n: int) -> np.ndarray:
+    _f32c(h, "h"), _f32c(g, "g"), _f32c(V, "V")
+    N, d = h.shape
+    r = V.shape[1]
+    if V.shape[0] != n:
+        raise ValueError("V must be [n, r]")
+    S = np.empty((N, num_rows(d, n), r), dtype=np.float32)
+    _check(_load().oracle_sketch(N, d, n, r, _ptr(h), _ptr(g), _ptr(V), _ptr(S)), "sketch")
+    return S
+
+
+def worker_sum(S: np.ndarray) -> np.ndarray:
+    _f32c(S, "S")
+    N, m, r = S.shape
+    P = np.empty((m, r), dtype=np.float32)
+    _check(_load().oracle_worker_sum(N, m, r, _ptr(S), _ptr(P)), "worker_sum")
+    return P
+
+
+def importance(P: np.ndarray) -> np.ndarray:
+    _f32c(P, "P")
+    m, r = P.shape
+    sigma = np.empty(m, dtype=np.float32)
+    _check(_load().oracle_importance(m, r, _ptr(P), _ptr(sigma)), "importance")
+    return sigma
+
+
+def _bucket_arrays(buckets):
+    if buckets is None:
+        return 0, None, None
+    begin = np.ascontiguousarray(np.asarray(buckets[0], dtype=np.int64))
+    kb = np.ascontiguousarray(np.asarray(buckets[1], dtype=np.int64))
+    if begin.shape[0] != kb.shape[0] + 1:
+        raise ValueError("bucket_row_begin must have num_buckets + 1 entries")
+    return kb.shape[0], begin, kb
+
+
+def select(sigma: np.ndarray, K: int = 0, buckets=None) -> np.ndarray:
+    """buckets = (row_begin[nb+1], K[nb]) or None for one global bucket."""
+    _f32c(sigma, "sigma")
+    m = sigma.shape[0]
+    nb, begin, kb = _bucket_arrays(buckets)
+    cap = m
+    idx = np.empty(cap, dtype=np.int32)
+    total = ctypes.c_int64(0)
+    _check(_load().oracle_select(m, _ptr(sigma), K, nb, _ptr(begin), _ptr(kb), _ptr(idx),
+                                 ctypes.addressof(total)), "select")
+    return idx[: total.value].copy()
+
+
+def gather_update(h: np.ndarray, g: np.ndarray, idx: np.ndarray, n: int) -> np.ndarray:
+    """Returns agg [K_total, n]; updates g in place."""
+    _f32c(h, "h"), _f32c(g, "g")
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    N, d = h.shape
+    agg = np.empty((idx.shape[0], n), dtype=np.float32)
+    _check(_load().oracle_gather_update(N, d, n, idx.shape[0], _ptr(idx), _ptr(h), _ptr(g),
+                                        _ptr(agg)), "gather_update")
+    return agg
+
+
+def step(h: np.ndarray, g: np.ndarray, grad: np.ndarray, *, n: int, r: int, eta: float,
+         seed: int, t: int, K: int = 0, buckets=None, V: np.ndarray | None = None,
+         want_sigma: bool = False, want_S: bool = False) -> dict:
+    """One compressor step; h and g are updated in place.
+
+    Returns {"idx": int32[K_total], "agg": float32[K_total, n]} plus "sigma" /
+    "S" when asked for.
+    """
+    _f32c(h, "h"), _f32c(g, "g")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    N, d = h.shape
+    if g.shape != h.shape or grad.shape != h.shape:
+        raise ValueError("h, g and grad must all be [N, d]")
+    m = num_rows(d, n)
+    nb, begin, kb = _bucket_arrays(buckets)
+    idx = np.empty(m, dtype=np.int32)
+    # Upper bound on the number of selected rows keeps the payload buffer small.
+    if nb == 0:
+        kmax = min(m, max(K, 0))
+    else:
+        kmax = int(sum(min(max(int(k), 0), int(b1 - b0))
+                       for k, b0, b1 in zip(kb, begin[:-1], begin[1:])))
+    agg = np.empty((max(kmax, 1), n), dtype=np.float32)
+    sigma = np.empty(m, dtype=np.float32) if want_sigma else None
+    S = np.empty((N, m, r), dtype=np.float32) if want_S else None
+    if V is not None:
+        V = np.ascontiguousarray(V, dtype=np.float32)
+        if V.shape != (n, r):
+            raise ValueError("V must be [n, r]")
+    total = ctypes.c_int64(0)
+    _check(_load().oracle_step(N, d, n, r, eta, seed & (2**64 - 1), t, K, nb, _ptr(begin),
+                               _ptr(kb), _ptr(grad), is_bf16, _ptr(h), _ptr(g), _ptr(idx),
+                               _ptr(agg), ctypes.addressof(total), _ptr(V), _ptr(sigma),
+                               _ptr(S)), "step")
+    k = total.value
+    out = {"idx": idx[:k].copy(), "agg": agg[:k].copy()}
+    if want_sigma:
+        out["sigma"] = sigma
+    if want_S:
+        out["S"] = S
+    return out

@@ -1,0 +1,342 @@
+/*
+ * arc_oracle.c -- plain CPU oracle of the ARC-Top-K + EF21M compressor step.
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by the tests, the smoke check and the
+ * benchmark's CPU-baseline leg.  It shares no code with libarctopk.
+ *
+ * Each function follows one step of the paper (arXiv:2510.26709) in the
+ * paper's order and notation; the comment above it names the passage.
+ * Arithmetic is IEEE binary32 with the explicit fmaf calls shown and nothing
+ * else contracted (build with -ffp-contract=off, no fast-math).  Sums run in
+ * the plain ascending order of their index.  The parallel loops only split
+ * independent outputs between threads; no output depends on the thread count.
+ */
+#include "arc_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* ---------------------------------------------------------------------------
+ * Shared random seed -> Gaussian projection V.
+ *
+ * Sec. IV ("Compressor Design") and Alg. 1: at iteration t all nodes agree on
+ * a seed s that deterministically generates V in R^{n x r} with
+ * vec(V) ~ N(0, I_{nr}).  The paper names no generator.  This oracle uses the
+ * SplitMix64 generator of Steele, Lea and Flood ("Fast splittable
+ * pseudorandom number generators", OOPSLA 2014): state starts at the seed and
+ * advances by the golden-gamma constant; each output is the state passed
+ * through the variant-13 mixing function.  Output x of the stream (0-based)
+ * is therefore mix(seed + (x + 1) * gamma).
+ *
+ * Entry V[j][k] uses the counter c = (t*n + j)*r + k: outputs 2c and 2c+1
+ * give u1 in (0,1] and u2 in [0,1) with 53 random bits each, and the
+ * Box-Muller transform (Box and Muller, 1958; cosine branch) gives
+ * z = sqrt(-2 ln u1) * cos(2 pi u2) in binary64, rounded once to binary32.
+ * ------------------------------------------------------------------------- */
+uint64_t oracle_splitmix64(uint64_t seed, uint64_t x) {
+  uint64_t z = seed + (x + 1u) * UINT64_C(0x9E3779B97F4A7C15);
+  z = (z ^ (z >> 30)) * UINT64_C(0xBF58476D1CE4E5B9);
+  z = (z ^ (z >> 27)) * UINT64_C(0x94D049BB133111EB);
+  return z ^ (z >> 31);
+}
+
+int oracle_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
+                      float *V) {
+  if (n < 1 || r < 1 || V == NULL) return 1;
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int64_t j = 0; j < n; ++j) {
+    for (int32_t k = 0; k < r; ++k) {
+      uint64_t c = ((uint64_t)t * (uint64_t)n + (uint64_t)j) * (uint64_t)r +
+                   (uint64_t)k;
+      uint64_t b1 = oracle_splitmix64(seed, 2u * c);
+      uint64_t b2 = oracle_splitmix64(seed, 2u * c + 1u);
+      double u1 = (double)((b1 >> 11) + 1u) * 0x1.0p-53; /* (0, 1] */
+      double u2 = (double)(b2 >> 11) * 0x1.0p-53;        /* [0, 1) */
+      double z = sqrt(-2.0 * log(u1)) * cos(two_pi * u2);
+      V[j * r + k] = (float)z;
+    }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * EF21M momentum, Eq. (11a):  h_t = (1 - eta) h_{t-1} + eta * grad.
+ * Binary32: a = fl(1 - eta); h = fmaf(eta, grad, fl(a * h)).
+ * bf16 gradients widen to binary32 exactly (the 16 bits become the high half).
+ * ------------------------------------------------------------------------- */
+static float grad_at(const void *grad, int32_t is_bf16, int64_t idx) {
+  if (is_bf16) {
+    uint32_t bits = (uint32_t)((const uint16_t *)grad)[idx] << 16;
+    float x;
+    memcpy(&x, &bits, sizeof x);
+    return x;
+  }
+  return ((const float *)grad)[idx];
+}
+
+int oracle_momentum(int32_t N, int64_t d, float eta, const void *grad,
+                    int32_t grad_is_bf16, float *h) {
+  if (N < 1 || d < 1 || grad == NULL || h == NULL) return 1;
+  if (!(eta >= 0.0f && eta <= 1.0f)) return 1;
+  const float a = 1.0f - eta;
+  const int64_t total = (int64_t)N * d;
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < total; ++e) {
+    float x = grad_at(grad, grad_is_bf16, e);
+    float ah = a * h[e];
+    h[e] = fmaf(eta, x, ah);
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Local sketch (Sec. IV and Alg. 1): P_t^{(i)} = G_t^{(i)} V, where G^{(i)} is
+ * the row-major m x n view (Eq. (3)) of the compressor's argument.  In EF21M
+ * (Eq. (11b)) that argument is the residual Delta^{(i)} = h_t^{(i)} -
+ * g_{t-1}^{(i)}, so element e of row p is fl(h[i][e] - g[i][e]).
+ * The 1/sqrt(r) factor of the text is left out, as in Alg. 1: a positive
+ * scale cannot change the arg-top-K.
+ * Dot product order: s = +0; s = fmaf(Delta[p*n + j], V[j][k], s) for
+ * j = 0, 1, ..., n-1, stopping at the end of the vector in a ragged last row.
+ * ------------------------------------------------------------------------- */
+int oracle_sketch(int32_t N, int64_t d, int64_t n, int32_t r, const float *h,
+                  const float *g, const float *V, float *S) {
+  if (N < 1 || d < 1 || n < 1 || r < 1) return 1;
+  if (h == NULL || g == NULL || V == NULL || S == NULL) return 1;
+  const int64_t m = ceil_div(d, n);
+  const int64_t rows = (int64_t)N * m;
+#pragma omp parallel for schedule(static)
+  for (int64_t ip = 0; ip < rows; ++ip) {
+    const int64_t i = ip / m, p = ip % m;
+    const float *hi = h + i * d, *gi = g + i * d;
+    for (int32_t k = 0; k < r; ++k) {
+      float s = 0.0f;
+      for (int64_t j = 0; j < n; ++j) {
+        const int64_t e = p * n + j;
+        if (e >= d) break;
+        const float delta = hi[e] - gi[e];
+        s = fmaf(delta, V[j * r + k], s);
+      }
+      S[ip * r + k] = s;
+    }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Sketch All-Reduce (Alg. 1): P = sum over workers of P^{(i)}.
+ * The paper writes a mean; the 1/N is left out because it cannot change the
+ * arg-top-K.  Order: P = S[0]; P = fl(P + S[i]) for i = 1, ..., N-1.
+ * ------------------------------------------------------------------------- */
+int oracle_worker_sum(int32_t N, int64_t m, int32_t r, const float *S,
+                      float *P) {
+  if (N < 1 || m < 1 || r < 1 || S == NULL || P == NULL) return 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t p = 0; p < m; ++p) {
+    for (int32_t k = 0; k < r; ++k) {
+      float acc = S[p * r + k];
+      for (int32_t i = 1; i < N; ++i) acc = acc + S[((int64_t)i * m + p) * r + k];
+      P[p * r + k] = acc;
+    }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Row importance, Eq. (4): Sigma = diag(P P^T), i.e. the squared Euclidean
+ * norm of each row of P.  Order: s = +0; s = fmaf(P[p][k], P[p][k], s) for
+ * k = 0, ..., r-1.
+ * ------------------------------------------------------------------------- */
+int oracle_importance(int64_t m, int32_t r, const float *P, float *sigma) {
+  if (m < 1 || r < 1 || P == NULL || sigma == NULL) return 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t p = 0; p < m; ++p) {
+    float s = 0.0f;
+    for (int32_t k = 0; k < r; ++k) s = fmaf(P[p * r + k], P[p * r + k], s);
+    sigma[p] = s;
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Eq. (4): I = arg top_K(Sigma), the K rows of largest importance.
+ * The paper does not say how ties are broken; here the lower row index wins,
+ * and the selected rows are returned in ascending order.  Sigma >= +0, so
+ * comparing the binary32 bit patterns as unsigned integers orders the values.
+ * K larger than the number of rows selects every row (alpha = K/m = 1, the
+ * identity compressor).  With buckets, each bucket [lo, hi) is an independent
+ * m x n block with its own K, and the per-bucket results are concatenated.
+ * Method: sort all rows of the bucket by (key descending, row ascending),
+ * keep the first K, sort those ascending.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  uint32_t key;
+  int32_t row;
+} keyed_row;
+
+static int by_key_desc_row_asc(const void *pa, const void *pb) {
+  const keyed_row *a = (const keyed_row *)pa, *b = (const keyed_row *)pb;
+  if (a->key != b->key) return a->key > b->key ? -1 : 1;
+  return (a->row > b->row) - (a->row < b->row);
+}
+
+static int by_int_asc(const void *pa, const void *pb) {
+  const int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+  return (a > b) - (a < b);
+}
+
+int oracle_select(int64_t m, const float *sigma, int64_t K_global,
+                  int32_t num_buckets, const int64_t *bucket_row_begin,
+                  const int64_t *bucket_K, int32_t *idx, int64_t *K_total) {
+  if (m < 1 || m > INT32_MAX || sigma == NULL || idx == NULL ||
+      K_total == NULL)
+    return 1;
+  int64_t one_begin[2] = {0, m};
+  int64_t one_K[1] = {K_global};
+  const int64_t *begin = one_begin, *Kb = one_K;
+  int32_t nb = 1;
+  if (num_buckets < 0) return 1;
+  if (num_buckets > 0) {
+    if (bucket_row_begin == NULL || bucket_K == NULL) return 1;
+    begin = bucket_row_begin;
+    Kb = bucket_K;
+    nb = num_buckets;
+    if (begin[0] != 0 || begin[nb] != m) return 1;
+    for (int32_t b = 0; b < nb; ++b)
+      if (begin[b + 1] <= begin[b]) return 1;
+  }
+  for (int32_t b = 0; b < nb; ++b)
+    if (Kb[b] < 0) return 1;
+
+  keyed_row *rows = (keyed_row *)malloc((size_t)m * sizeof(keyed_row));
+  if (rows == NULL) return 1;
+  int64_t out = 0;
+  for (int32_t b = 0; b < nb; ++b) {
+    const int64_t lo = begin[b], hi = begin[b + 1], cnt = hi - lo;
+    int64_t k = Kb[b] < cnt ? Kb[b] : cnt;
+    for (int64_t p = lo; p < hi; ++p) {
+      uint32_t bits;
+      memcpy(&bits, &sigma[p], sizeof bits);
+      rows[p - lo].key = bits;
+      rows[p - lo].row = (int32_t)p;
+    }
+    qsort(rows, (size_t)cnt, sizeof(keyed_row), by_key_desc_row_asc);
+    for (int64_t q = 0; q < k; ++q) idx[out + q] = rows[q].row;
+    qsort(idx + out, (size_t)k, sizeof(int32_t), by_int_asc);
+    out += k;
+  }
+  free(rows);
+  *K_total = out;
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Row gather and payload All-Reduce (Eq. (5), Alg. 1 last steps) with the
+ * error-feedback update of Eq. (11b).
+ * C_local(Delta^{(i)}) keeps rows I of Delta^{(i)} = h_t^{(i)} - g_{t-1}^{(i)}
+ * and zeroes the others; every node uses the same I, so the sum over nodes
+ * needs no indices.  For each selected row p = I[q] and column j < n with
+ * e = p*n + j < d:
+ *   Delta_i = fl(h[i][e] - g[i][e])                      (same bits as before)
+ *   agg[q][j] = Delta_0 + Delta_1 + ... + Delta_{N-1}     (ascending i)
+ *   g[i][e]   = fl(g[i][e] + Delta_i)                     (Eq. (11b))
+ * agg is the sum over nodes (Alg. 1's output line); the mean of Eq. (5) is
+ * agg / N.  Columns past d in a ragged last row give agg = +0.
+ * ------------------------------------------------------------------------- */
+int oracle_gather_update(int32_t N, int64_t d, int64_t n, int64_t K_total,
+                         const int32_t *idx, const float *h, float *g,
+                         float *agg) {
+  if (N < 1 || d < 1 || n < 1 || K_total < 0) return 1;
+  if (K_total > 0 && (idx == NULL || h == NULL || g == NULL || agg == NULL))
+    return 1;
+  const int64_t m = ceil_div(d, n);
+  for (int64_t q = 0; q < K_total; ++q)
+    if (idx[q] < 0 || idx[q] >= m) return 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t q = 0; q < K_total; ++q) {
+    const int64_t p = idx[q];
+    for (int64_t j = 0; j < n; ++j) {
+      const int64_t e = p * n + j;
+      if (e >= d) {
+        agg[q * n + j] = 0.0f;
+        continue;
+      }
+      float acc = 0.0f;
+      for (int32_t i = 0; i < N; ++i) {
+        const int64_t at = (int64_t)i * d + e;
+        const float delta = h[at] - g[at];
+        acc = (i == 0) ? delta : acc + delta;
+        g[at] = g[at] + delta;
+      }
+      agg[q * n + j] = acc;
+    }
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * One compressor step: Eq. (11a), then Alg. 1 applied to Delta = h_t -
+ * g_{t-1}, then Eq. (11b).  The model update Eq. (11c) lies outside the
+ * compressor and is not part of this step.
+ * ------------------------------------------------------------------------- */
+int oracle_step(int32_t N, int64_t d, int64_t n, int32_t r, float eta,
+                uint64_t seed, int64_t t, int64_t K_global,
+                int32_t num_buckets, const int64_t *bucket_row_begin,
+                const int64_t *bucket_K, const void *grad,
+                int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                float *agg, int64_t *K_total, const float *V_override,
+                float *sigma_out, float *S_out) {
+  if (N < 1 || d < 1 || n < 1 || r < 1 || K_total == NULL) return 1;
+  const int64_t m = ceil_div(d, n);
+  if (m > INT32_MAX) return 1;
+  int rc = 1;
+  float *V = (float *)malloc((size_t)(n * r) * sizeof(float));
+  float *S = S_out ? S_out : (float *)malloc((size_t)((int64_t)N * m * r) * sizeof(float));
+  float *P = (float *)malloc((size_t)(m * r) * sizeof(float));
+  float *sigma = sigma_out ? sigma_out : (float *)malloc((size_t)m * sizeof(float));
+  if (V == NULL || S == NULL || P == NULL || sigma == NULL) goto done;
+
+  if (V_override)
+    memcpy(V, V_override, (size_t)(n * r) * sizeof(float));
+  else if (oracle_projection(seed, t, n, r, V))
+    goto done;
+  /* Reject a bad selection configuration before any state is touched. */
+  if (num_buckets < 0 || (num_buckets == 0 && K_global < 0)) goto done;
+  if (num_buckets > 0) {
+    if (bucket_row_begin == NULL || bucket_K == NULL) goto done;
+    if (bucket_row_begin[0] != 0 || bucket_row_begin[num_buckets] != m)
+      goto done;
+    for (int32_t b = 0; b < num_buckets; ++b)
+      if (bucket_row_begin[b + 1] <= bucket_row_begin[b] || bucket_K[b] < 0)
+        goto done;
+  }
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) goto done;
+  if (oracle_sketch(N, d, n, r, h, g, V, S)) goto done;
+  if (oracle_worker_sum(N, m, r, S, P)) goto done;
+  if (oracle_importance(m, r, P, sigma)) goto done;
+  if (oracle_select(m, sigma, K_global, num_buckets, bucket_row_begin,
+                    bucket_K, idx, K_total))
+    goto done;
+  if (oracle_gather_update(N, d, n, *K_total, idx, h, g, agg)) goto done;
+  rc = 0;
+done:
+  free(V);
+  if (!S_out) free(S);
+  free(P);
+  if (!sigma_out) free(sigma);
+  return rc;
+}

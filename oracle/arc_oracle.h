@@ -1,0 +1,92 @@
+/*
+ * arc_oracle.h -- plain CPU oracle of the ARC-Top-K + EF21M compressor step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  The product path
+ * (libarctopk) never links, loads or calls it, and the two share no code.
+ *
+ * Paper: C. Chen, C. Ma, Z. Li, Y. He, Y. Dong, K. Yuan, "An All-Reduce
+ * Compatible Top-K Compressor for Communication-Efficient Distributed
+ * Learning", arXiv:2510.26709.  Equation numbers follow the paper's own
+ * numbering: (3) reshape g -> G, (4) row importance and arg-top-K,
+ * (5) row aggregation, (6) unbiasedness of the importance, (11a)-(11c) the
+ * EF21M recursion; "Alg. 1" is the ARC-Top-K algorithm box of Sec. IV.
+ *
+ * Precision: the paper fixes none.  The arg-top-K turns floating point into
+ * an integer decision, so this oracle takes that decision in the same
+ * precision as the GPU path: IEEE binary32, every operation correctly
+ * rounded, in the fixed sequential order documented on each function, with
+ * no contraction other than the explicit fmaf calls.
+ *
+ * Layout: worker i's d-vector occupies elements [i*d, (i+1)*d) of an [N][d]
+ * array; its m x n view (Eq. (3)) is row-major, row p = elements
+ * [p*n, p*n + n) clipped at d, with m = ceil(d / n).  Elements past d in the
+ * last row are absent (they take part in no sum and are never written).
+ *
+ * All functions return 0 on success and 1 on an invalid argument.
+ */
+#ifndef ARC_ORACLE_H
+#define ARC_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Gaussian projection V (n x r, row-major V[j*r + k]) for seed s, step t. */
+int oracle_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
+                      float *V);
+
+/* SplitMix64: output number x (0-based) of the stream seeded with `seed`. */
+uint64_t oracle_splitmix64(uint64_t seed, uint64_t x);
+
+/* EF21M momentum, Eq. (11a), in place on h[N*d].  grad is fp32
+ * (grad_is_bf16 == 0) or bf16 bit patterns (grad_is_bf16 == 1). */
+int oracle_momentum(int32_t N, int64_t d, float eta, const void *grad,
+                    int32_t grad_is_bf16, float *h);
+
+/* Per-worker sketch S[i][p][k] of the residual h - g (Alg. 1, local
+ * projection), S is [N][m][r]. */
+int oracle_sketch(int32_t N, int64_t d, int64_t n, int32_t r, const float *h,
+                  const float *g, const float *V, float *S);
+
+/* Worker sum P[p][k] over i (Alg. 1, first All-Reduce), P is [m][r]. */
+int oracle_worker_sum(int32_t N, int64_t m, int32_t r, const float *S,
+                      float *P);
+
+/* Row importance sigma[p] = sum_k P[p][k]^2 (Eq. (4), diag(P P^T)). */
+int oracle_importance(int64_t m, int32_t r, const float *P, float *sigma);
+
+/* Per-bucket arg-top-K of sigma (Eq. (4)); ties to the lower row, output
+ * ascending within a bucket, buckets concatenated in order.  num_buckets == 0
+ * means one bucket [0, m) with K = K_global.  Returns the number of indices
+ * written through *K_total. */
+int oracle_select(int64_t m, const float *sigma, int64_t K_global,
+                  int32_t num_buckets, const int64_t *bucket_row_begin,
+                  const int64_t *bucket_K, int32_t *idx, int64_t *K_total);
+
+/* Gather + worker sum + error-feedback update at the shared rows (Eq. (5),
+ * Alg. 1 second All-Reduce, Eq. (11b)).  agg is [K_total][n]. */
+int oracle_gather_update(int32_t N, int64_t d, int64_t n, int64_t K_total,
+                         const int32_t *idx, const float *h, float *g,
+                         float *agg);
+
+/* One full compressor step: momentum, sketch, worker sum, importance,
+ * selection, gather/update.  V_override (n*r floats) replaces the generated
+ * projection when non-NULL.  sigma_out ([m]) and S_out ([N][m][r]) are
+ * optional copies of the intermediates. */
+int oracle_step(int32_t N, int64_t d, int64_t n, int32_t r, float eta,
+                uint64_t seed, int64_t t, int64_t K_global,
+                int32_t num_buckets, const int64_t *bucket_row_begin,
+                const int64_t *bucket_K, const void *grad,
+                int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                float *agg, int64_t *K_total, const float *V_override,
+                float *sigma_out, float *S_out);
+
+/* Number of threads the oracle's parallel loops use. */
+int oracle_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
