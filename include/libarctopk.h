@@ -1,0 +1,183 @@
+/*
+ * libarctopk -- the ARC-Top-K + EF21M compressor step on one AMD Instinct
+ * MI355X (gfx950), behind a plain C ABI.
+ *
+ * Method: C. Chen, C. Ma, Z. Li, Y. He, Y. Dong, K. Yuan, "An All-Reduce
+ * Compatible Top-K Compressor for Communication-Efficient Distributed
+ * Learning", arXiv:2510.26709.  Equation numbers are the paper's: (3) the
+ * reshape g -> G (m x n), (4) row importance Sigma = diag(P P^T) and
+ * I = arg top_K(Sigma), (5) the row aggregation, (11a)/(11b) the EF21M
+ * momentum and error-feedback lines.  "Alg. 1" is the ARC-Top-K algorithm box
+ * of Sec. IV.
+ *
+ * The N data-parallel nodes of the paper are simulated as the leading axis of
+ * an [N][d] batch on one GPU.  One call of arc_step performs, for step t:
+ *
+ *   h^(i)   <- (1 - eta) h^(i) + eta grad^(i)                       (11a)
+ *   Delta^(i) = h^(i) - g^(i)      (the compressor's argument in (11b))
+ *   V_t     = n x r Gaussian matrix from (seed, t)           (Sec. IV, Alg. 1)
+ *   P       = sum_i Delta^(i)_{m x n} V_t                        (Alg. 1)
+ *   Sigma_p = ||P_p||^2,  I = arg top_K(Sigma)                        (4)
+ *   agg     = sum_i rows I of Delta^(i)  (packed, index-free payload; (5))
+ *   g^(i)   <- g^(i) + (rows I of Delta^(i))                        (11b)
+ *
+ * Numerics (the contract shared with the reference CPU implementation):
+ * binary32 everywhere; every sum in ascending index order; the dot products
+ * over a row and the squares in Sigma use fused multiply-add chains starting
+ * at +0; the worker sums are plain additions in ascending worker order; V_t
+ * is rounded once from a binary64 Box-Muller value.  Ties in Sigma go to the
+ * lower row.  With these rules the selected rows are exactly reproducible.
+ * The 1/sqrt(r) and 1/N factors of the text are not applied: they cannot
+ * change I, and agg is the SUM over workers (divide by N for the mean of (5)).
+ *
+ * Layout: worker i's vector is elements [i*d, (i+1)*d) of each [N][d] array.
+ * Row p of its m x n view (row-major, Eq. (3)) is elements [p*n, p*n + n)
+ * clipped at d; m = ceil(d / n).  Elements past d in a ragged last row do
+ * not exist: they are never read or written and give +0 in agg.
+ *
+ * Streams: all device work of a context is enqueued on the HIP stream given
+ * to arc_create.  arc_step returns after enqueueing; its outputs are valid
+ * once that stream has completed the work.  A context is not thread-safe; use
+ * one per stream.  Preconditions: finite inputs (non-finite values give
+ * unspecified selections).
+ *
+ * Errors: every entry point returns an arc_status.  Invalid arguments are
+ * detected before any device work is enqueued and leave all buffers
+ * untouched.  After ARC_ERR_DEVICE the context must be destroyed.
+ * arc_last_error() gives a human-readable reason for the last failure on the
+ * calling thread.
+ */
+#ifndef LIBARCTOPK_H
+#define LIBARCTOPK_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct arc_ctx arc_ctx;
+
+typedef enum {
+  ARC_OK = 0,
+  ARC_ERR_INVALID = 1,     /* bad argument or configuration                  */
+  ARC_ERR_NOMEM = 2,       /* device or pinned host allocation failed        */
+  ARC_ERR_DEVICE = 3,      /* HIP runtime or launch failure                  */
+  ARC_ERR_UNSUPPORTED = 4  /* valid request this build does not implement    */
+} arc_status;
+
+typedef enum { ARC_DTYPE_F32 = 0, ARC_DTYPE_BF16 = 1 } arc_dtype;
+
+/* Largest projection dimension r accepted. */
+#define ARC_MAX_R 32
+
+/*
+ * Problem description (Alg. 1 inputs, EF21M step size, shared seed).
+ *   d            coordinates per worker (> 0)
+ *   n            row width of the m x n view (> 0); m = ceil(d/n) <= 2^31-1
+ *   K            selected ROWS when num_buckets == 0 (>= 0; K >= m keeps
+ *                every row, i.e. the identity compressor).  The paper's
+ *                K = ceil(mu * m) for a compression ratio mu.
+ *   seed         shared seed s; V_t is a function of (seed, t) only
+ *   bucket_row_begin, bucket_K
+ *                optional independent selections (num_buckets > 0): bucket b
+ *                is rows [bucket_row_begin[b], bucket_row_begin[b+1]) with its
+ *                own K (bucket_K[b] >= 0, clamped to the bucket's rows).
+ *                bucket_row_begin has num_buckets+1 strictly increasing
+ *                entries from 0 to m.  Host arrays, copied by arc_create.
+ *   N            workers (> 0)
+ *   r            projection dimension, 1..ARC_MAX_R (the paper uses 4)
+ *   grad_dtype   arc_dtype of the gradients; h and g are always binary32
+ *   num_buckets  0 for one global selection over all m rows
+ *   eta          EF21M momentum weight, 0 <= eta <= 1
+ */
+typedef struct {
+  int64_t d;
+  int64_t n;
+  int64_t K;
+  uint64_t seed;
+  const int64_t *bucket_row_begin;
+  const int64_t *bucket_K;
+  int32_t N;
+  int32_t r;
+  int32_t grad_dtype;
+  int32_t num_buckets;
+  float eta;
+  int32_t reserved; /* must be 0 */
+} arc_config;
+
+/*
+ * Validate cfg, allocate the device workspace (projection, per-worker sketch,
+ * importance, selection scratch) on the current HIP device and bind the
+ * context to `hip_stream` (a hipStream_t; NULL = the default stream).
+ * On failure *out is set to NULL.  Workspace bytes are about
+ * 4*(n*r + N*m*r + 3*m) plus a few kilobytes per bucket.
+ */
+arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
+
+/*
+ * One compressor step t (t >= 0 selects V_t).  Device pointers:
+ *   grad     [N*d] gradients (grad_dtype), read only; must not overlap h or g
+ *   h        [N*d] binary32 momentum, read and written (Eq. (11a))
+ *   g        [N*d] binary32 error-feedback state; rows in I are updated
+ *            (Eq. (11b)), all other elements are left bit-for-bit unchanged
+ *   out_idx  [K_total] int32: the selected rows, ascending within each bucket,
+ *            buckets in order
+ *   out_agg  [K_total*n] binary32: row q holds sum_i Delta^(i) of row
+ *            out_idx[q] (ascending worker order); +0 past d
+ * K_total = arc_selected_rows(ctx).  out_idx / out_agg may be NULL only when
+ * K_total == 0.  Pointers 16-byte aligned with d % 4 == 0 and n % 32 == 0
+ * take the vectorised path; anything else takes a slower path with identical
+ * results.
+ */
+arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
+                    float *g, int32_t *out_idx, float *out_agg);
+
+/* Release the context and its workspace.  NULL is accepted.  Waits for the
+ * context's stream to finish its work first. */
+arc_status arc_destroy(arc_ctx *ctx);
+
+/* Rows of the m x n view (m = ceil(d/n)); -1 for NULL. */
+int64_t arc_num_rows(const arc_ctx *ctx);
+
+/* Rows selected per step after clamping each K to its bucket; -1 for NULL. */
+int64_t arc_selected_rows(const arc_ctx *ctx);
+
+/* Static string naming a status code. */
+const char *arc_status_str(arc_status s);
+
+/* Reason for the most recent failure on the calling thread ("" if none). */
+const char *arc_last_error(void);
+
+/* ---- Inspection hooks (tests and benchmarks; not needed by the method) ---- */
+
+/* Enqueue a copy of the last step's importance Sigma ([m] binary32) into the
+ * device buffer out_sigma. */
+arc_status arc_debug_sigma(arc_ctx *ctx, float *out_sigma);
+
+/* Enqueue a copy of the last step's per-worker sketch S ([N][m][r] binary32,
+ * S[i][p][k] = sum_j Delta^(i)[p*n+j] V[j][k]) into the device buffer out_S. */
+arc_status arc_debug_sketch(arc_ctx *ctx, float *out_S);
+
+/* Write V_t ([n][r] binary32, row-major) for step t into host memory out_V,
+ * exactly as arc_step would use it (honours arc_set_projection). */
+arc_status arc_debug_projection(arc_ctx *ctx, int64_t t, float *out_V);
+
+/* Use the host matrix V ([n][r] binary32, copied) for every later step
+ * instead of V_t; NULL restores the seeded projection. */
+arc_status arc_set_projection(arc_ctx *ctx, const float *V);
+
+/* Stage timing: when enabled, arc_step records HIP events on the context's
+ * stream around its stages.  arc_timing_read waits for those events and
+ * writes, for each of the ARC_NUM_STAGES stages, the summed milliseconds
+ * (ms[stage]) over the steps recorded since the last read (*steps); then it
+ * clears the record.  Stages: 0 streaming sketch (momentum + residual +
+ * per-worker sketch), 1 worker sum + importance, 2 top-K selection, 3 gather +
+ * worker sum + error-feedback update, 4 the whole step. */
+#define ARC_NUM_STAGES 5
+arc_status arc_timing_enable(arc_ctx *ctx, int32_t on);
+arc_status arc_timing_read(arc_ctx *ctx, double *ms, int64_t *steps);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

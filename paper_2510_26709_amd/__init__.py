@@ -1,0 +1,68 @@
+"""libarctopk: the ARC-Top-K + EF21M compressor step (arXiv:2510.26709) as
+hand-written HIP kernels for the AMD Instinct MI355X (gfx950).
+
+The library is the C ABI declared in ``include/libarctopk.h``; this package is
+its ctypes binding (same entry-point names) plus ``Compressor``, a small owner
+of a context and its output buffers.  All compute runs in ``libarctopk.so``.
+"""
+from __future__ import annotations
+
+from ._lib import (  # noqa: F401
+    ARC_DTYPE_BF16, ARC_DTYPE_F32, ARC_ERR_DEVICE, ARC_ERR_INVALID, ARC_ERR_NOMEM,
+    ARC_ERR_UNSUPPORTED, ARC_MAX_R, ARC_NUM_STAGES, ARC_OK, EXPORTED, LIB_PATH, STAGE_NAMES,
+    ArcError, arc_config, arc_create, arc_debug_projection, arc_debug_sigma, arc_debug_sketch,
+    arc_destroy, arc_last_error, arc_num_rows, arc_selected_rows, arc_set_projection,
+    arc_status_str, arc_step, arc_timing_enable, arc_timing_read, make_config)
+
+
+class Compressor:
+    """One libarctopk context bound to a torch stream, with its outputs.
+
+    ``step(t, grad, h, g)`` enqueues one compressor step and returns the
+    device tensors (idx [K_total] int32, agg [K_total, n] float32); they are
+    overwritten by the next step.
+    """
+
+    def __init__(self, *, d, N, n, r=4, K=0, eta, seed, grad_dtype="f32", buckets=None,
+                 device=None, stream=None):
+        import torch
+        self.device = torch.device(device or "cuda")
+        self.stream = stream or torch.cuda.current_stream(self.device)
+        dt = ARC_DTYPE_BF16 if grad_dtype == "bf16" else ARC_DTYPE_F32
+        cfg, keep = make_config(d=d, N=N, n=n, r=r, K=K, eta=eta, seed=seed, grad_dtype=dt,
+                                buckets=buckets)
+        with torch.cuda.device(self.device):
+            self.ctx = arc_create(cfg, self.stream)
+        del keep
+        self.d, self.N, self.n, self.r = d, N, n, r
+        self.m = arc_num_rows(self.ctx)
+        self.K_total = arc_selected_rows(self.ctx)
+        self.idx = torch.empty(max(self.K_total, 1), dtype=torch.int32, device=self.device)
+        self.agg = torch.empty((max(self.K_total, 1), n), dtype=torch.float32, device=self.device)
+
+    def step(self, t, grad, h, g):
+        arc_step(self.ctx, t, grad, h, g, self.idx, self.agg)
+        return self.idx[: self.K_total], self.agg[: self.K_total]
+
+    def sigma(self):
+        import torch
+        out = torch.empty(self.m, dtype=torch.float32, device=self.device)
+        arc_debug_sigma(self.ctx, out)
+        return out
+
+    def sketch(self):
+        import torch
+        out = torch.empty((self.N, self.m, self.r), dtype=torch.float32, device=self.device)
+        arc_debug_sketch(self.ctx, out)
+        return out
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            arc_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,451 @@
+// libarctopk C ABI: configuration checks, device workspace, and the per-step
+// enqueue of the ARC-Top-K + EF21M pipeline on the caller's HIP stream.
+#include <hip/hip_runtime.h>
+
+#include <array>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "arc_internal.h"
+#include "libarctopk.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+arc_status fail(arc_status s, const std::string& why) {
+  g_last_error = why;
+  return s;
+}
+
+arc_status fail_hip(hipError_t e, const char* where) {
+  g_last_error = std::string(where) + ": " + hipGetErrorString(e);
+  return e == hipErrorOutOfMemory ? ARC_ERR_NOMEM : ARC_ERR_DEVICE;
+}
+
+#define ARC_HIP(call, where)                          \
+  do {                                                \
+    const hipError_t arc_e_ = (call);                 \
+    if (arc_e_ != hipSuccess) return fail_hip(arc_e_, where); \
+  } while (0)
+
+constexpr int kEventsPerStep = 6;
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
+  const uintptr_t pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
+
+}  // namespace
+
+struct arc_ctx {
+  // problem
+  int64_t d = 0, n = 0, m = 0, m_full = 0;
+  int32_t N = 0, r = 0, grad_bf16 = 0;
+  float eta = 0.f, a = 0.f;
+  uint64_t seed = 0;
+  int64_t K_total = 0;
+  std::vector<arc::BucketDesc> buckets;
+  std::vector<arc::BlockDesc> blocks;
+  // device
+  hipStream_t stream = nullptr;
+  int device = 0;
+  float* V_dev = nullptr;
+  float* S_dev = nullptr;
+  float* sigma_dev = nullptr;
+  arc::BucketDesc* buckets_dev = nullptr;
+  arc::BlockDesc* blocks_dev = nullptr;
+  arc::BucketState* state_dev = nullptr;
+  uint32_t* ghist_dev = nullptr;
+  uint32_t* counter_dev = nullptr;
+  uint32_t* blockcnt_dev = nullptr;
+  uint32_t* blockbase_dev = nullptr;
+  // projection staging: two pinned buffers, reused every other step
+  float* V_pinned[2] = {nullptr, nullptr};
+  hipEvent_t V_done[2] = {nullptr, nullptr};
+  bool V_pending[2] = {false, false};
+  int V_slot = 0;
+  std::vector<float> V_override;
+  bool use_override = false;
+  // stage timing
+  bool timing = false;
+  std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
+  size_t ev_used = 0;
+
+  arc::SelectWorkspace select_ws() const {
+    arc::SelectWorkspace ws;
+    ws.buckets = buckets_dev;
+    ws.blocks = blocks_dev;
+    ws.state = state_dev;
+    ws.ghist = ghist_dev;
+    ws.counter = counter_dev;
+    ws.blockcnt = blockcnt_dev;
+    ws.blockbase = blockbase_dev;
+    ws.nb = static_cast<int32_t>(buckets.size());
+    ws.nblk = static_cast<int32_t>(blocks.size());
+    return ws;
+  }
+
+  void release() {
+    (void)hipStreamSynchronize(stream);
+    for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
+                    static_cast<void*>(sigma_dev), static_cast<void*>(buckets_dev),
+                    static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
+                    static_cast<void*>(ghist_dev), static_cast<void*>(counter_dev),
+                    static_cast<void*>(blockcnt_dev), static_cast<void*>(blockbase_dev)})
+      if (p) (void)hipFree(p);
+    for (int s = 0; s < 2; ++s) {
+      if (V_done[s]) (void)hipEventDestroy(V_done[s]);
+      if (V_pinned[s]) (void)hipHostFree(V_pinned[s]);
+    }
+    for (auto& evs : ev_pool)
+      for (hipEvent_t e : evs)
+        if (e) (void)hipEventDestroy(e);
+    ev_pool.clear();
+  }
+};
+
+namespace {
+
+// Configuration checks shared by arc_create; no HIP call is made here.
+arc_status check_config(const arc_config* cfg, int64_t* m_out) {
+  if (cfg == nullptr) return fail(ARC_ERR_INVALID, "cfg is NULL");
+  if (cfg->d <= 0) return fail(ARC_ERR_INVALID, "d must be > 0");
+  if (cfg->n <= 0) return fail(ARC_ERR_INVALID, "n must be > 0");
+  if (cfg->N <= 0 || cfg->N > 65535) return fail(ARC_ERR_INVALID, "N must be in 1..65535");
+  if (cfg->r <= 0 || cfg->r > ARC_MAX_R) return fail(ARC_ERR_INVALID, "r must be in 1..ARC_MAX_R");
+  if (cfg->grad_dtype != ARC_DTYPE_F32 && cfg->grad_dtype != ARC_DTYPE_BF16)
+    return fail(ARC_ERR_INVALID, "grad_dtype must be ARC_DTYPE_F32 or ARC_DTYPE_BF16");
+  if (!(cfg->eta >= 0.0f && cfg->eta <= 1.0f)) return fail(ARC_ERR_INVALID, "eta must be in [0, 1]");
+  if (cfg->reserved != 0) return fail(ARC_ERR_INVALID, "reserved must be 0");
+  if (cfg->d > INT64_MAX / cfg->N) return fail(ARC_ERR_INVALID, "N*d overflows");
+  const int64_t m = cfg->d / cfg->n + (cfg->d % cfg->n != 0);
+  if (m > INT32_MAX) return fail(ARC_ERR_INVALID, "m = ceil(d/n) exceeds 2^31-1");
+  if (cfg->num_buckets < 0) return fail(ARC_ERR_INVALID, "num_buckets must be >= 0");
+  if (cfg->num_buckets == 0) {
+    if (cfg->K < 0) return fail(ARC_ERR_INVALID, "K must be >= 0");
+  } else {
+    if (cfg->bucket_row_begin == nullptr || cfg->bucket_K == nullptr)
+      return fail(ARC_ERR_INVALID, "bucket arrays are NULL");
+    if (cfg->bucket_row_begin[0] != 0 || cfg->bucket_row_begin[cfg->num_buckets] != m)
+      return fail(ARC_ERR_INVALID, "buckets must cover rows [0, m)");
+    for (int32_t b = 0; b < cfg->num_buckets; ++b) {
+      if (cfg->bucket_row_begin[b + 1] <= cfg->bucket_row_begin[b])
+        return fail(ARC_ERR_INVALID, "bucket_row_begin must be strictly increasing");
+      if (cfg->bucket_K[b] < 0) return fail(ARC_ERR_INVALID, "bucket_K must be >= 0");
+    }
+  }
+  *m_out = m;
+  return ARC_OK;
+}
+
+void build_selection_plan(const arc_config* cfg, arc_ctx* c) {
+  const int32_t nb = cfg->num_buckets == 0 ? 1 : cfg->num_buckets;
+  int64_t out = 0;
+  for (int32_t b = 0; b < nb; ++b) {
+    arc::BucketDesc bd{};
+    bd.lo = cfg->num_buckets == 0 ? 0 : cfg->bucket_row_begin[b];
+    bd.hi = cfg->num_buckets == 0 ? c->m : cfg->bucket_row_begin[b + 1];
+    const int64_t want = cfg->num_buckets == 0 ? cfg->K : cfg->bucket_K[b];
+    bd.k = want < bd.hi - bd.lo ? want : bd.hi - bd.lo;
+    bd.out_off = out;
+    bd.mode = bd.k == 0 ? arc::kSelectNone
+              : bd.k == bd.hi - bd.lo ? arc::kSelectAll : arc::kSelectRadix;
+    bd.first_blk = static_cast<int32_t>(c->blocks.size());
+    for (int64_t lo = bd.lo; lo < bd.hi; lo += arc::kRowsPerSelectBlock) {
+      arc::BlockDesc blk{};
+      blk.lo = lo;
+      blk.hi = lo + arc::kRowsPerSelectBlock < bd.hi ? lo + arc::kRowsPerSelectBlock : bd.hi;
+      blk.bucket = b;
+      c->blocks.push_back(blk);
+    }
+    bd.nblk = static_cast<int32_t>(c->blocks.size()) - bd.first_blk;
+    out += bd.k;
+    c->buckets.push_back(bd);
+  }
+  c->K_total = out;
+}
+
+template <typename T>
+arc_status dev_alloc(T** p, size_t count, const char* what) {
+  if (count == 0) count = 1;
+  const hipError_t e = hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail_hip(e, what);
+  }
+  return ARC_OK;
+}
+
+arc_status record(arc_ctx* c, size_t slot, int which) {
+  if (!c->timing) return ARC_OK;
+  ARC_HIP(hipEventRecord(c->ev_pool[slot][which], c->stream), "hipEventRecord");
+  return ARC_OK;
+}
+
+// Pinned staging + async copy of this step's projection.
+arc_status upload_projection(arc_ctx* c, int64_t t) {
+  const int s = c->V_slot;
+  c->V_slot ^= 1;
+  if (c->V_pending[s]) {
+    ARC_HIP(hipEventSynchronize(c->V_done[s]), "hipEventSynchronize(projection)");
+    c->V_pending[s] = false;
+  }
+  const size_t count = static_cast<size_t>(c->n) * c->r;
+  if (c->use_override)
+    std::memcpy(c->V_pinned[s], c->V_override.data(), count * sizeof(float));
+  else
+    arc::generate_projection(c->seed, t, c->n, c->r, c->V_pinned[s]);
+  ARC_HIP(hipMemcpyAsync(c->V_dev, c->V_pinned[s], count * sizeof(float),
+                         hipMemcpyHostToDevice, c->stream),
+          "hipMemcpyAsync(projection)");
+  ARC_HIP(hipEventRecord(c->V_done[s], c->stream), "hipEventRecord(projection)");
+  c->V_pending[s] = true;
+  return ARC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* arc_status_str(arc_status s) {
+  switch (s) {
+    case ARC_OK: return "ARC_OK";
+    case ARC_ERR_INVALID: return "ARC_ERR_INVALID";
+    case ARC_ERR_NOMEM: return "ARC_ERR_NOMEM";
+    case ARC_ERR_DEVICE: return "ARC_ERR_DEVICE";
+    case ARC_ERR_UNSUPPORTED: return "ARC_ERR_UNSUPPORTED";
+  }
+  return "ARC_ERR_UNKNOWN";
+}
+
+const char* arc_last_error(void) { return g_last_error.c_str(); }
+
+arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
+  if (out == nullptr) return fail(ARC_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  int64_t m = 0;
+  arc_status st = check_config(cfg, &m);
+  if (st != ARC_OK) return st;
+
+  arc_ctx* c = new (std::nothrow) arc_ctx();
+  if (c == nullptr) return fail(ARC_ERR_NOMEM, "host allocation failed");
+  try {
+    c->d = cfg->d;
+    c->n = cfg->n;
+    c->m = m;
+    c->m_full = cfg->d / cfg->n;
+    c->N = cfg->N;
+    c->r = cfg->r;
+    c->grad_bf16 = cfg->grad_dtype == ARC_DTYPE_BF16;
+    c->eta = cfg->eta;
+    c->a = 1.0f - cfg->eta;
+    c->seed = cfg->seed;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    build_selection_plan(cfg, c);
+  } catch (...) {
+    delete c;
+    return fail(ARC_ERR_NOMEM, "host allocation failed");
+  }
+
+  auto bail = [&](arc_status s) {
+    c->release();
+    delete c;
+    return s;
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return bail(fail_hip(e, "hipGetDevice"));
+
+  const size_t nb = c->buckets.size(), nblk = c->blocks.size();
+  if ((st = dev_alloc(&c->V_dev, static_cast<size_t>(c->n) * c->r, "hipMalloc(V)")) ||
+      (st = dev_alloc(&c->S_dev, static_cast<size_t>(c->N) * c->m * c->r, "hipMalloc(S)")) ||
+      (st = dev_alloc(&c->sigma_dev, static_cast<size_t>(c->m), "hipMalloc(sigma)")) ||
+      (st = dev_alloc(&c->buckets_dev, nb, "hipMalloc(buckets)")) ||
+      (st = dev_alloc(&c->blocks_dev, nblk, "hipMalloc(blocks)")) ||
+      (st = dev_alloc(&c->state_dev, nb, "hipMalloc(state)")) ||
+      (st = dev_alloc(&c->ghist_dev, nb * arc::kRadixBins, "hipMalloc(hist)")) ||
+      (st = dev_alloc(&c->counter_dev, 4, "hipMalloc(counter)")) ||
+      (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")) ||
+      (st = dev_alloc(&c->blockbase_dev, 2 * nblk, "hipMalloc(blockbase)")))
+    return bail(st);
+  for (int s = 0; s < 2; ++s) {
+    e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
+                      static_cast<size_t>(c->n) * c->r * sizeof(float), hipHostMallocDefault);
+    if (e != hipSuccess) {
+      c->V_pinned[s] = nullptr;
+      return bail(fail_hip(e, "hipHostMalloc(projection)"));
+    }
+    e = hipEventCreateWithFlags(&c->V_done[s], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      c->V_done[s] = nullptr;
+      return bail(fail_hip(e, "hipEventCreate"));
+    }
+  }
+  // Constant selection tables, and zeroed radix scratch (kept zero between
+  // uses by the kernels themselves).
+  e = hipMemcpy(c->buckets_dev, c->buckets.data(), nb * sizeof(arc::BucketDesc),
+                hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(c->blocks_dev, c->blocks.data(), nblk * sizeof(arc::BlockDesc),
+                  hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemset(c->ghist_dev, 0, nb * arc::kRadixBins * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(c->counter_dev, 0, 4 * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) return bail(fail_hip(e, "workspace initialisation"));
+  *out = c;
+  return ARC_OK;
+}
+
+arc_status arc_destroy(arc_ctx* ctx) {
+  if (ctx == nullptr) return ARC_OK;
+  ctx->release();
+  delete ctx;
+  return ARC_OK;
+}
+
+int64_t arc_num_rows(const arc_ctx* ctx) { return ctx ? ctx->m : -1; }
+
+int64_t arc_selected_rows(const arc_ctx* ctx) { return ctx ? ctx->K_total : -1; }
+
+arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                    int32_t* out_idx, float* out_agg) {
+  if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
+  if (t < 0) return fail(ARC_ERR_INVALID, "t must be >= 0");
+  if (grad == nullptr || h == nullptr || g == nullptr)
+    return fail(ARC_ERR_INVALID, "grad, h and g must be non-NULL");
+  if (c->K_total > 0 && (out_idx == nullptr || out_agg == nullptr))
+    return fail(ARC_ERR_INVALID, "out_idx and out_agg must be non-NULL");
+  const size_t elems = static_cast<size_t>(c->N) * static_cast<size_t>(c->d);
+  const size_t grad_bytes = elems * (c->grad_bf16 ? 2 : 4), state_bytes = elems * 4;
+  if (ranges_overlap(grad, grad_bytes, h, state_bytes) ||
+      ranges_overlap(grad, grad_bytes, g, state_bytes) ||
+      ranges_overlap(h, state_bytes, g, state_bytes))
+    return fail(ARC_ERR_INVALID, "grad, h and g must not overlap");
+
+  const bool vec_ok = c->n % 32 == 0 && c->d % 4 == 0 && aligned16(grad) &&
+                      aligned16(h) && aligned16(g);
+  const bool fast_sketch = vec_ok && (c->r == 1 || c->r == 2 || c->r == 4 || c->r == 8);
+  const bool fast_gather = c->n % 4 == 0 && c->d % 4 == 0 && aligned16(h) &&
+                           aligned16(g) && aligned16(out_agg);
+
+  size_t slot = 0;
+  if (c->timing) {
+    if (c->ev_used == c->ev_pool.size()) {
+      std::array<hipEvent_t, kEventsPerStep> evs{};
+      for (auto& e : evs) ARC_HIP(hipEventCreate(&e), "hipEventCreate");
+      c->ev_pool.push_back(evs);
+    }
+    slot = c->ev_used++;
+  }
+  arc_status st;
+  if ((st = record(c, slot, 0))) return st;
+  if ((st = upload_projection(c, t))) return st;
+  if ((st = record(c, slot, 1))) return st;
+  // Stage 0: momentum + residual + per-worker sketch (one HBM stream).
+  const int64_t fast_rows = fast_sketch ? c->m_full : 0;
+  ARC_HIP(arc::launch_sketch(fast_sketch, grad, c->grad_bf16, h, g, c->V_dev,
+                             c->S_dev, c->d, c->n, c->m, c->N, c->r, 0, fast_rows,
+                             c->eta, c->a, c->stream),
+          "sketch launch");
+  ARC_HIP(arc::launch_sketch(false, grad, c->grad_bf16, h, g, c->V_dev, c->S_dev, c->d,
+                             c->n, c->m, c->N, c->r, fast_rows, c->m, c->eta, c->a,
+                             c->stream),
+          "sketch launch (general rows)");
+  if ((st = record(c, slot, 2))) return st;
+  // Stage 1: worker sum + importance.
+  const arc::SelectWorkspace ws = c->select_ws();
+  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->m, c->N, c->r, ws,
+                                        c->stream),
+          "reduce launch");
+  if ((st = record(c, slot, 3))) return st;
+  // Stage 2: per-bucket top-K.
+  ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
+  if ((st = record(c, slot, 4))) return st;
+  // Stage 3: gather + worker sum + error-feedback update.
+  ARC_HIP(arc::launch_gather_update(fast_gather, h, g, out_idx, out_agg, c->K_total,
+                                    c->d, c->n, c->m, c->N, c->stream),
+          "gather launch");
+  if ((st = record(c, slot, 5))) return st;
+  return ARC_OK;
+}
+
+arc_status arc_debug_sigma(arc_ctx* c, float* out_sigma) {
+  if (c == nullptr || out_sigma == nullptr) return fail(ARC_ERR_INVALID, "NULL argument");
+  ARC_HIP(hipMemcpyAsync(out_sigma, c->sigma_dev, static_cast<size_t>(c->m) * sizeof(float),
+                         hipMemcpyDeviceToDevice, c->stream),
+          "hipMemcpyAsync(sigma)");
+  return ARC_OK;
+}
+
+arc_status arc_debug_sketch(arc_ctx* c, float* out_S) {
+  if (c == nullptr || out_S == nullptr) return fail(ARC_ERR_INVALID, "NULL argument");
+  ARC_HIP(hipMemcpyAsync(out_S, c->S_dev,
+                         static_cast<size_t>(c->N) * c->m * c->r * sizeof(float),
+                         hipMemcpyDeviceToDevice, c->stream),
+          "hipMemcpyAsync(S)");
+  return ARC_OK;
+}
+
+arc_status arc_debug_projection(arc_ctx* c, int64_t t, float* out_V) {
+  if (c == nullptr || out_V == nullptr) return fail(ARC_ERR_INVALID, "NULL argument");
+  if (t < 0) return fail(ARC_ERR_INVALID, "t must be >= 0");
+  if (c->use_override)
+    std::memcpy(out_V, c->V_override.data(), c->V_override.size() * sizeof(float));
+  else
+    arc::generate_projection(c->seed, t, c->n, c->r, out_V);
+  return ARC_OK;
+}
+
+arc_status arc_set_projection(arc_ctx* c, const float* V) {
+  if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
+  if (V == nullptr) {
+    c->use_override = false;
+    c->V_override.clear();
+    return ARC_OK;
+  }
+  try {
+    c->V_override.assign(V, V + static_cast<size_t>(c->n) * c->r);
+  } catch (...) {
+    return fail(ARC_ERR_NOMEM, "host allocation failed");
+  }
+  c->use_override = true;
+  return ARC_OK;
+}
+
+arc_status arc_timing_enable(arc_ctx* c, int32_t on) {
+  if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
+  c->timing = on != 0;
+  return ARC_OK;
+}
+
+arc_status arc_timing_read(arc_ctx* c, double* ms, int64_t* steps) {
+  if (c == nullptr || ms == nullptr || steps == nullptr)
+    return fail(ARC_ERR_INVALID, "NULL argument");
+  for (int k = 0; k < ARC_NUM_STAGES; ++k) ms[k] = 0.0;
+  for (size_t s = 0; s < c->ev_used; ++s) {
+    auto& ev = c->ev_pool[s];
+    ARC_HIP(hipEventSynchronize(ev[kEventsPerStep - 1]), "hipEventSynchronize");
+    float x = 0.f;
+    const int pairs[ARC_NUM_STAGES][2] = {{1, 2}, {2, 3}, {3, 4}, {4, 5}, {0, 5}};
+    for (int k = 0; k < ARC_NUM_STAGES; ++k) {
+      ARC_HIP(hipEventElapsedTime(&x, ev[pairs[k][0]], ev[pairs[k][1]]),
+              "hipEventElapsedTime");
+      ms[k] += x;
+    }
+  }
+  *steps = static_cast<int64_t>(c->ev_used);
+  c->ev_used = 0;
+  return ARC_OK;
+}
+
+}  // extern "C"

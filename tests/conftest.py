@@ -15,15 +15,19 @@ def pytest_configure(config):
 
 def _ensure_built():
     # Load what is built; build only what is missing (a fresh checkout).
-    from oracle import build as ob
+    import torch  # noqa: F401  (first: the process then holds torch's HIP runtime)
+    import __graft_entry__ as ge
+    ob = ge._load_by_path("_arc_oracle_build", "oracle/build.py")
     if not os.path.exists(ob.LIB):
         ob.build_oracle()
-    try:
-        from synth import build as sb
-    except ImportError:
-        return
+    sb = ge._load_by_path("_arc_synth_build", "synth/build.py")
     if not os.path.exists(sb.HOST_LIB):
         sb.build_synth_host()
+    if not os.path.exists(sb.DEV_LIB):
+        sb.build_synth_dev()
+    lb = ge._load_by_path("_arc_lib_build", "paper_2510_26709_amd/build.py")
+    if not os.path.exists(lb.LIB):
+        lb.build_lib()
 
 
 _ensure_built()

@@ -1,0 +1,160 @@
+"""GPU parity of libarctopk against the CPU oracle on small seeded cases that
+span several tiles, ragged tails, every kernel path and the degenerate cases
+of the method (K = 0, K >= m, all-equal importance, buckets)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2510_26709_amd as arc
+import synth
+from parity_util import log, run_case
+
+pytestmark = pytest.mark.gpu
+F32 = np.float32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+# name, kwargs.  "fast" = vectorised sketch (n % 32 == 0, d % 4 == 0, r in 1/2/4/8)
+CASES = [
+    ("fast_f32_ragged", dict(d=256 * 700 + 40, N=3, n=256, r=4, K=9, steps=3)),
+    ("fast_bf16_ragged", dict(d=512 * 300 + 8, N=4, n=512, r=4, K=5, steps=3,
+                              grad_dtype="bf16", family=1)),
+    ("fast_r1", dict(d=64 * 999, N=2, n=64, r=1, K=30, steps=2)),
+    ("fast_r2", dict(d=96 * 513, N=5, n=96, r=2, K=7, steps=2)),
+    ("fast_r8", dict(d=32 * 4097, N=2, n=32, r=8, K=100, steps=2)),
+    ("fast_many_tiles", dict(d=768 * 2600, N=8, n=768, r=4, K=3, steps=2)),
+    ("generic_n100_r3", dict(d=100 * 321 + 7, N=3, n=100, r=3, K=12, steps=2)),
+    ("generic_odd_d", dict(d=32 * 200 + 3, N=2, n=32, r=4, K=6, steps=2)),
+    ("generic_r5_bf16", dict(d=64 * 300, N=2, n=64, r=5, K=4, steps=2, grad_dtype="bf16",
+                             family=1)),
+    ("n1_exact_like", dict(d=5000, N=3, n=1, r=4, K=50, steps=2)),
+    ("k_zero", dict(d=256 * 50, N=2, n=256, r=4, K=0, steps=2)),
+    ("k_all", dict(d=256 * 50 + 4, N=2, n=256, r=4, K=51, steps=2)),
+    ("k_over", dict(d=256 * 50, N=2, n=256, r=4, K=10_000, steps=2)),
+    ("k_one", dict(d=256 * 3000, N=4, n=256, r=4, K=1, steps=2)),
+    ("single_worker", dict(d=128 * 640, N=1, n=128, r=4, K=20, steps=2)),
+    ("eta_one", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=1.0, steps=2)),
+    ("eta_zero", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=0.0, steps=2)),
+    ("select_multiblock", dict(d=32 * 9000, N=2, n=32, r=4, K=2500, steps=2)),
+]
+
+
+@pytest.mark.parametrize("name,kw", CASES, ids=[c[0] for c in CASES])
+def test_parity_small(name, kw):
+    log(f"[parity] {name} {kw}")
+    run_case(label=name, check_S=True, **kw)
+
+
+def test_parity_misaligned_pointers_take_the_general_path():
+    log("[parity] misaligned")
+    run_case(label="misaligned", d=256 * 120, N=3, n=256, r=4, K=11, steps=2, misalign=1)
+
+
+def test_parity_buckets():
+    # buckets: radix, dense (K >= rows), empty selection, one-row bucket
+    n = 64
+    begin = [0, 1000, 1300, 1301, 5000, 6000]
+    ks = [17, 500, 1, 0, 10]
+    d = n * 6000
+    log("[parity] buckets")
+    run_case(label="buckets", d=d, N=3, n=n, r=4, buckets=(begin, ks), steps=3)
+
+
+def test_parity_zero_residual_ties_take_lowest_rows():
+    d, N, n = 256 * 400, 2, 256
+    zero = np.zeros((N, d), F32)
+    log("[parity] zero residual")
+    run_case(label="zeros", d=d, N=N, n=n, K=13, steps=2, grad_fn=lambda t: zero)
+
+
+def test_parity_crafted_ties():
+    # V = ones (r = 1): Sigma_p = (sum over workers and row of Delta)^2, built
+    # from small integers so that many rows tie exactly at the threshold.
+    d, N, n = 32 * 5000, 2, 32
+    rng = np.random.default_rng(5)
+    vals = rng.integers(0, 4, size=(5000,)).astype(F32)  # row sums in {0..3}
+
+    def grad(t):
+        g = np.zeros((N, d), F32)
+        g[0, ::n] = vals  # first column of each row for worker 0
+        return g
+
+    log("[parity] crafted ties")
+    run_case(label="ties", d=d, N=N, n=n, r=1, K=1234, eta=1.0, steps=1, grad_fn=grad,
+             V=np.ones((n, 1), F32))
+
+
+def test_parity_injected_projection():
+    rng = np.random.default_rng(9)
+    V = rng.standard_normal((256, 4)).astype(F32)
+    log("[parity] injected V")
+    run_case(label="injected_V", d=256 * 333, N=3, n=256, K=10, steps=2, V=V)
+
+
+def test_library_projection_matches_oracle_bitwise():
+    comp = arc.Compressor(d=768 * 10, N=1, n=768, r=4, K=1, eta=0.1, seed=2003)
+    try:
+        for t in (0, 1, 19, 123456):
+            got = np.empty((768, 4), F32)
+            arc.arc_debug_projection(comp.ctx, t, got)
+            want = oracle.projection(2003, t, 768, 4)
+            assert got.tobytes() == want.tobytes(), t
+    finally:
+        comp.close()
+
+
+def test_repeat_is_bit_identical():
+    # Same inputs twice: every output identical (no scheduling dependence).
+    d, N, n, K = 512 * 2000, 4, 512, 40
+    gen = synth.Generator(d, N, 3)
+    grad = torch.from_numpy(gen.fill_host(0)).cuda()
+    outs = []
+    for _ in range(2):
+        comp = arc.Compressor(d=d, N=N, n=n, K=K, eta=0.1, seed=5)
+        h = torch.zeros((N, d), device="cuda")
+        g = torch.zeros((N, d), device="cuda")
+        idx, agg = comp.step(0, grad, h, g)
+        sig = comp.sigma()
+        torch.cuda.synchronize()
+        outs.append([x.cpu().numpy().tobytes() for x in (idx, agg, sig, h, g)])
+        comp.close()
+    assert outs[0] == outs[1]
+
+
+def test_step_rejects_overlapping_buffers():
+    d, N = 256 * 10, 2
+    comp = arc.Compressor(d=d, N=N, n=256, K=2, eta=0.1, seed=5)
+    try:
+        h = torch.zeros((N, d), device="cuda")
+        g = torch.zeros((N, d), device="cuda")
+        with pytest.raises(arc.ArcError, match="overlap"):
+            arc.arc_step(comp.ctx, 0, h, h, g, comp.idx, comp.agg)
+        with pytest.raises(arc.ArcError, match="overlap"):
+            arc.arc_step(comp.ctx, 0, g, h, g, comp.idx, comp.agg)
+        with pytest.raises(arc.ArcError, match="t must be"):
+            arc.arc_step(comp.ctx, -1, torch.zeros_like(h), h, g, comp.idx, comp.agg)
+    finally:
+        comp.close()
+
+
+def test_device_generator_matches_host_generator():
+    for kw in (dict(d=1 << 20, N=3, seed=1001, per_coord_scale=True, noise=0.3),
+               dict(d=11_689_512 // 8, N=2, seed=1002, noise=0.5, scale_sigma=1.5,
+                    boost=20.0, boost_frac=0.001),
+               dict(d=2048 * 300, N=4, seed=1004, grad_dtype="bf16", family=1,
+                    tensors=[2048 * 100, 2048 * 150, 2048 * 50])):
+        gen = synth.Generator(**kw)
+        for t in (0, 3):
+            dt = torch.int16 if gen.grad_dtype == "bf16" else torch.float32
+            out = torch.empty((gen.N, gen.d), dtype=dt, device="cuda")
+            gen.fill_device(t, out)
+            torch.cuda.synchronize()
+            dev_np = out.cpu().numpy().view(gen.np_dtype)
+            host_np = gen.fill_host(t)
+            assert dev_np.tobytes() == host_np.tobytes(), (kw, t)
