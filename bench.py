@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Throughput of one ARC-Top-K + EF21M compressor step (libarctopk) on one MI355X.
+
+A step is one pass of the whole path over one [N, d] batch of synthetic
+gradients already resident in HBM: momentum, residual, per-worker sketch,
+worker sum, importance, top-K selection, gather + worker sum + error-feedback
+update.  Prints ONE JSON line:
+
+  value        gradient elements per second, N*d / (time per step)
+  roofline     the streaming sketch kernel (the dominant one): algorithmic
+               bytes per launch / its mean duration (HIP events on the
+               library's stream over the timed region) against 8 TB/s
+  cpu_baseline the CPU oracle on a bounded prefix of the same workload
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
+DEFAULT_WORKLOAD = "llama1b"    # the 1.1B-parameter configuration
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sketch_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2510_26709_amd", "csrc", "arc_kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w, K_total):
+    """Bytes the method must move per step (each array touched once)."""
+    bg = w.bytes_per_grad
+    Nd = w.N * w.d
+    stream = Nd * (bg + 12)                         # grad + h read/write + g read
+    sketch_out = 4 * w.N * w.m * w.r                # per-worker sketch written
+    reduce_ = 4 * w.N * w.m * w.r + 4 * w.m         # sketch read, importance written
+    select = 4 * 4 * w.m                            # importance read by 4 passes
+    gather = K_total * w.n * (12 * w.N + 4)         # h, g read, g written, agg written
+    return {"sketch_kernel": stream + sketch_out, "step": stream + sketch_out + reduce_ +
+            select + gather + 4 * K_total}
+
+
+def kernel_traffic(w):
+    """HBM bytes per launch of the sketch kernel from committed rocprofv3
+    counters, if they were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(KERNEL_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+        entry = rec.get("workloads", {}).get(w.name)
+        if rec.get("kernel_source_sha256") != sha or entry is None:
+            return None
+        return float(entry["hbm_bytes_per_launch"])
+    except (OSError, ValueError, KeyError):
+        return None
+
+
+def cpu_baseline(w, grads_dev, seconds_target=12.0):
+    """Time the CPU oracle on a prefix of the workload: the first m_s rows of
+    every worker's vector (d_s = m_s * n), K scaled to the same ratio, from
+    h = g = 0, on the same synthetic gradients (copied from the device)."""
+    import numpy as np
+
+    import oracle
+    threads = oracle.num_threads()
+
+    def run(rows, steps):
+        d_s = rows * w.n
+        K_s = max(1, math.ceil(w.mu * rows))
+        h = np.zeros((w.N, d_s), np.float32)
+        g = np.zeros((w.N, d_s), np.float32)
+        grads = []
+        for s in range(steps):
+            gd = grads_dev[s % len(grads_dev)][:, :d_s].contiguous().cpu().numpy()
+            grads.append(gd.view(np.uint16) if w.grad_dtype == "bf16" else gd)
+        t0 = time.perf_counter()
+        for s in range(steps):
+            oracle.step(h, g, grads[s], n=w.n, r=w.r, eta=w.eta, seed=w.sketch_seed, t=s, K=K_s)
+        return (time.perf_counter() - t0) / steps, d_s, K_s
+
+    # calibrate on a small prefix, then size the sample to the time target
+    rows0 = max(1, min(w.m, (1 << 22) // w.n))
+    t1, _, _ = run(rows0, 1)
+    per_row = t1 / rows0
+    steps = 2
+    rows = int(min(w.m, max(rows0, seconds_target / steps / max(per_row, 1e-12))))
+    if rows == w.m:  # whole workload fits the time budget: spend it on more steps
+        steps = int(max(2, min(8, seconds_target / max(per_row * rows, 1e-9))))
+    t_step, d_s, K_s = run(rows, steps)
+    return {
+        "value": w.N * d_s / t_step,
+        "unit": "gradient elements/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"first {rows} of {w.m} rows per worker (d={d_s}, N={w.N}, n={w.n}, "
+                   f"K={K_s} rows), {steps} steps from h=g=0, mean s/step={t_step:.3f}"),
+    }
+
+
+def copy_calibration(torch, gib, reps):
+    """Plain device-to-device copy of a known size: every launch reads and
+    writes `gib` GiB exactly once."""
+    nbytes = int(gib * 2**30) // 16 * 16
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    end.record()
+    end.synchronize()
+    ms = start.elapsed_time(end) / reps
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps,
+                      "ms_per_copy": ms, "GBps_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}),
+          flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--batches", type=int, default=4,
+                    help="distinct gradient batches kept resident and cycled")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="instead of the compressor, time a plain device copy of GIB "
+                         "gibibytes (empirical bandwidth ceiling; counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X: the compressor path here is single-GPU "
+              "(workers are simulated on the device); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration > 0:
+        copy_calibration(torch, args.copy_calibration, max(args.steps, 1))
+        return
+
+    import paper_2510_26709_amd as arc
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(dev)
+    gen = synth.Generator.for_workload(w)
+    gdt = torch.int16 if w.grad_dtype == "bf16" else torch.float32
+    nb = max(1, min(args.batches, args.steps + args.warmup))
+    log(f"[bench] workload={w.name} d={w.d} N={w.N} n={w.n} r={w.r} grad={w.grad_dtype} "
+        f"batches={nb}")
+    with torch.cuda.stream(stream):
+        grads = []
+        for b in range(nb):
+            x = torch.empty((w.N, w.d), dtype=gdt, device=dev)
+            gen.fill_device(b, x, stream)
+            grads.append(x)
+        h = torch.zeros((w.N, w.d), dtype=torch.float32, device=dev)
+        g = torch.zeros((w.N, w.d), dtype=torch.float32, device=dev)
+        comp = arc.Compressor(d=w.d, N=w.N, n=w.n, r=w.r, K=w.K_global(), eta=w.eta,
+                              seed=w.sketch_seed, grad_dtype=w.grad_dtype,
+                              buckets=w.buckets(), device=dev, stream=stream)
+        stream.synchronize()
+        log(f"[bench] m={comp.m} K_total={comp.K_total}; {comp.describe()}; warmup {args.warmup}")
+        for t in range(args.warmup):
+            comp.step(t, grads[t % nb], h, g)
+        stream.synchronize()
+        arc.arc_timing_enable(comp.ctx, True)
+        arc.arc_timing_read(comp.ctx)  # clear
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for k in range(args.steps):
+            t = args.warmup + k
+            comp.step(t, grads[t % nb], h, g)
+        end.record(stream)
+        end.synchronize()
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+        stage_ms, nsteps = arc.arc_timing_read(comp.ctx)
+        arc.arc_timing_enable(comp.ctx, False)
+    ms_per_step = total_ms / args.steps
+    stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
+    log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
+
+    byt = algorithmic_bytes(w, comp.K_total)
+    sk_ms = stages["sketch"]
+    achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
+    traffic = kernel_traffic(w)
+    value = w.N * w.d / (ms_per_step * 1e-3)
+    step_gbps = byt["step"] / (ms_per_step * 1e-3) / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        cpu = cpu_baseline(w, grads)
+        log(f"[bench] cpu baseline {cpu['value']:.3e} elements/s on {cpu['cores']} threads")
+    comp_desc = comp.describe()
+    comp.close()
+
+    out = {
+        "metric": "arc_step gradient elements/s (1 MI355X)",
+        "value": value,
+        "unit": "gradient elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "d": w.d, "N": w.N, "n": w.n, "r": w.r, "m": comp.m,
+                   "K_rows": comp.K_total, "grad_dtype": w.grad_dtype, "eta": w.eta,
+                   "mu": w.mu, "buckets": 0 if w.buckets() is None else len(w.buckets()[1])},
+        "step_hbm_GBps": step_gbps,
+        "step_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
+        "stage_ms": stages,
+        "path": comp_desc,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "sketch_fast_kernel (momentum + residual + per-worker sketch)",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": byt["sketch_kernel"],
+            "mean_launch_ms": sk_ms,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

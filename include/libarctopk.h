@@ -150,6 +150,12 @@ const char *arc_last_error(void);
 
 /* ---- Inspection hooks (tests and benchmarks; not needed by the method) ---- */
 
+/* Write a one-line, NUL-terminated description of how the context runs a
+ * step for pointers that take the vectorised path (kernel variants, LDS per
+ * block and the device limit, selection blocks) into buf (at most len bytes,
+ * truncated).  Host only. */
+arc_status arc_describe(const arc_ctx *ctx, char *buf, int64_t len);
+
 /* Enqueue a copy of the last step's importance Sigma ([m] binary32) into the
  * device buffer out_sigma. */
 arc_status arc_debug_sigma(arc_ctx *ctx, float *out_sigma);

@@ -10,7 +10,7 @@ from __future__ import annotations
 from ._lib import (  # noqa: F401
     ARC_DTYPE_BF16, ARC_DTYPE_F32, ARC_ERR_DEVICE, ARC_ERR_INVALID, ARC_ERR_NOMEM,
     ARC_ERR_UNSUPPORTED, ARC_MAX_R, ARC_NUM_STAGES, ARC_OK, EXPORTED, LIB_PATH, STAGE_NAMES,
-    ArcError, arc_config, arc_create, arc_debug_projection, arc_debug_sigma, arc_debug_sketch,
+    ArcError, arc_config, arc_create, arc_debug_projection, arc_describe, arc_debug_sigma, arc_debug_sketch,
     arc_destroy, arc_last_error, arc_num_rows, arc_selected_rows, arc_set_projection,
     arc_status_str, arc_step, arc_timing_enable, arc_timing_read, make_config)
 
@@ -43,6 +43,9 @@ class Compressor:
     def step(self, t, grad, h, g):
         arc_step(self.ctx, t, grad, h, g, self.idx, self.agg)
         return self.idx[: self.K_total], self.agg[: self.K_total]
+
+    def describe(self):
+        return arc_describe(self.ctx)
 
     def sigma(self):
         import torch

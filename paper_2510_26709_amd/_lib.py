@@ -63,6 +63,7 @@ _SIGS = {
     "arc_selected_rows": (ctypes.c_int64, [_vp]),
     "arc_status_str": (ctypes.c_char_p, [_st]),
     "arc_last_error": (ctypes.c_char_p, []),
+    "arc_describe": (_st, [_vp, ctypes.c_char_p, ctypes.c_int64]),
     "arc_debug_sigma": (_st, [_vp, _vp]),
     "arc_debug_sketch": (_st, [_vp, _vp]),
     "arc_debug_projection": (_st, [_vp, ctypes.c_int64, _vp]),
@@ -156,6 +157,12 @@ def arc_status_str(status: int) -> str:
 
 def arc_last_error() -> str:
     return _lib.arc_last_error().decode()
+
+
+def arc_describe(ctx) -> str:
+    buf = ctypes.create_string_buffer(512)
+    _check(_lib.arc_describe(ctx, buf, len(buf)), "arc_describe")
+    return buf.value.decode()
 
 
 def arc_debug_sigma(ctx, out_sigma) -> None:

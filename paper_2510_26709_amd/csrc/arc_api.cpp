@@ -5,6 +5,7 @@
 #include <array>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
 #include <new>
 #include <string>
@@ -65,10 +66,9 @@ struct arc_ctx {
   arc::BucketDesc* buckets_dev = nullptr;
   arc::BlockDesc* blocks_dev = nullptr;
   arc::BucketState* state_dev = nullptr;
-  uint32_t* ghist_dev = nullptr;
-  uint32_t* counter_dev = nullptr;
+  uint32_t* hist_dev = nullptr;
   uint32_t* blockcnt_dev = nullptr;
-  uint32_t* blockbase_dev = nullptr;
+  size_t max_lds_per_block = 0;
   // projection staging: two pinned buffers, reused every other step
   float* V_pinned[2] = {nullptr, nullptr};
   hipEvent_t V_done[2] = {nullptr, nullptr};
@@ -86,12 +86,16 @@ struct arc_ctx {
     ws.buckets = buckets_dev;
     ws.blocks = blocks_dev;
     ws.state = state_dev;
-    ws.ghist = ghist_dev;
-    ws.counter = counter_dev;
+    ws.hist = hist_dev;
     ws.blockcnt = blockcnt_dev;
-    ws.blockbase = blockbase_dev;
     ws.nb = static_cast<int32_t>(buckets.size());
     ws.nblk = static_cast<int32_t>(blocks.size());
+    ws.any_radix = 0;
+    ws.any_output = 0;
+    for (const auto& b : buckets) {
+      ws.any_radix |= b.mode == arc::kSelectRadix;
+      ws.any_output |= b.mode != arc::kSelectNone;
+    }
     return ws;
   }
 
@@ -100,8 +104,7 @@ struct arc_ctx {
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
                     static_cast<void*>(sigma_dev), static_cast<void*>(buckets_dev),
                     static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
-                    static_cast<void*>(ghist_dev), static_cast<void*>(counter_dev),
-                    static_cast<void*>(blockcnt_dev), static_cast<void*>(blockbase_dev)})
+                    static_cast<void*>(hist_dev), static_cast<void*>(blockcnt_dev)})
       if (p) (void)hipFree(p);
     for (int s = 0; s < 2; ++s) {
       if (V_done[s]) (void)hipEventDestroy(V_done[s]);
@@ -160,11 +163,20 @@ void build_selection_plan(const arc_config* cfg, arc_ctx* c) {
     bd.out_off = out;
     bd.mode = bd.k == 0 ? arc::kSelectNone
               : bd.k == bd.hi - bd.lo ? arc::kSelectAll : arc::kSelectRadix;
+    // Fat blocks (few blocks per bucket keep the per-bin atomics and the
+    // block-prefix sums short), at most kMaxBlocksPerBucket of them.
+    const int64_t rows = bd.hi - bd.lo;
+    const int64_t per_block_cap =
+        (int64_t)arc::kSelectThreads * arc::kMaxBlocksPerBucket;
+    int64_t rpt = (rows + per_block_cap - 1) / per_block_cap;
+    if (rpt < arc::kMinRowsPerThread) rpt = arc::kMinRowsPerThread;
+    const int64_t rows_per_block = rpt * arc::kSelectThreads;
+    bd.rows_per_thread = rpt;
     bd.first_blk = static_cast<int32_t>(c->blocks.size());
-    for (int64_t lo = bd.lo; lo < bd.hi; lo += arc::kRowsPerSelectBlock) {
+    for (int64_t lo = bd.lo; lo < bd.hi; lo += rows_per_block) {
       arc::BlockDesc blk{};
       blk.lo = lo;
-      blk.hi = lo + arc::kRowsPerSelectBlock < bd.hi ? lo + arc::kRowsPerSelectBlock : bd.hi;
+      blk.hi = lo + rows_per_block < bd.hi ? lo + rows_per_block : bd.hi;
       blk.bucket = b;
       c->blocks.push_back(blk);
     }
@@ -273,11 +285,15 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
       (st = dev_alloc(&c->buckets_dev, nb, "hipMalloc(buckets)")) ||
       (st = dev_alloc(&c->blocks_dev, nblk, "hipMalloc(blocks)")) ||
       (st = dev_alloc(&c->state_dev, nb, "hipMalloc(state)")) ||
-      (st = dev_alloc(&c->ghist_dev, nb * arc::kRadixBins, "hipMalloc(hist)")) ||
-      (st = dev_alloc(&c->counter_dev, 4, "hipMalloc(counter)")) ||
-      (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")) ||
-      (st = dev_alloc(&c->blockbase_dev, 2 * nblk, "hipMalloc(blockbase)")))
+      (st = dev_alloc(&c->hist_dev, arc::kRadixPasses * nb * arc::kRadixBins,
+                      "hipMalloc(hist)")) ||
+      (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")))
     return bail(st);
+  int lds_limit = 0;
+  e = hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock,
+                            c->device);
+  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
+  c->max_lds_per_block = static_cast<size_t>(lds_limit);
   for (int s = 0; s < 2; ++s) {
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
                       static_cast<size_t>(c->n) * c->r * sizeof(float), hipHostMallocDefault);
@@ -298,8 +314,9 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   if (e == hipSuccess)
     e = hipMemcpy(c->blocks_dev, c->blocks.data(), nblk * sizeof(arc::BlockDesc),
                   hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemset(c->ghist_dev, 0, nb * arc::kRadixBins * sizeof(uint32_t));
-  if (e == hipSuccess) e = hipMemset(c->counter_dev, 0, 4 * sizeof(uint32_t));
+  if (e == hipSuccess)
+    e = hipMemset(c->hist_dev, 0,
+                  arc::kRadixPasses * nb * arc::kRadixBins * sizeof(uint32_t));
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) return bail(fail_hip(e, "workspace initialisation"));
   *out = c;
@@ -351,23 +368,33 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
   if ((st = record(c, slot, 0))) return st;
   if ((st = upload_projection(c, t))) return st;
   if ((st = record(c, slot, 1))) return st;
-  // Stage 0: momentum + residual + per-worker sketch (one HBM stream).
+  // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
+  // the same kernel also forms the worker sum and importance of its rows.
   const int64_t fast_rows = fast_sketch ? c->m_full : 0;
-  ARC_HIP(arc::launch_sketch(fast_sketch, grad, c->grad_bf16, h, g, c->V_dev,
-                             c->S_dev, c->d, c->n, c->m, c->N, c->r, 0, fast_rows,
-                             c->eta, c->a, c->stream),
-          "sketch launch");
+  const bool fused = fast_sketch && c->N <= arc::kMaxFusedWorkers &&
+                     arc::fused_sketch_lds_bytes(c->N) <= c->max_lds_per_block;
+  if (fused) {
+    ARC_HIP(arc::launch_sketch_fused(grad, c->grad_bf16, h, g, c->V_dev, c->S_dev,
+                                     c->sigma_dev, c->d, c->n, c->m, c->N, c->r, 0,
+                                     fast_rows, c->eta, c->a, c->stream),
+            "fused sketch launch");
+  } else {
+    ARC_HIP(arc::launch_sketch(fast_sketch, grad, c->grad_bf16, h, g, c->V_dev,
+                               c->S_dev, c->d, c->n, c->m, c->N, c->r, 0, fast_rows,
+                               c->eta, c->a, c->stream),
+            "sketch launch");
+  }
   ARC_HIP(arc::launch_sketch(false, grad, c->grad_bf16, h, g, c->V_dev, c->S_dev, c->d,
                              c->n, c->m, c->N, c->r, fast_rows, c->m, c->eta, c->a,
                              c->stream),
           "sketch launch (general rows)");
   if ((st = record(c, slot, 2))) return st;
-  // Stage 1: worker sum + importance.
-  const arc::SelectWorkspace ws = c->select_ws();
-  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->m, c->N, c->r, ws,
-                                        c->stream),
+  // Stage 1: worker sum + importance for the rows the fused kernel did not do.
+  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->m, c->N, c->r,
+                                        fused ? fast_rows : 0, c->m, c->stream),
           "reduce launch");
   if ((st = record(c, slot, 3))) return st;
+  const arc::SelectWorkspace ws = c->select_ws();
   // Stage 2: per-bucket top-K.
   ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
   if ((st = record(c, slot, 4))) return st;
@@ -376,6 +403,25 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
                                     c->d, c->n, c->m, c->N, c->stream),
           "gather launch");
   if ((st = record(c, slot, 5))) return st;
+  return ARC_OK;
+}
+
+arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
+  if (c == nullptr || buf == nullptr || len <= 0) return fail(ARC_ERR_INVALID, "NULL argument");
+  const bool vec_shape = c->n % 32 == 0 && c->d % 4 == 0 &&
+                         (c->r == 1 || c->r == 2 || c->r == 4 || c->r == 8);
+  const bool fused = vec_shape && c->N <= arc::kMaxFusedWorkers &&
+                     arc::fused_sketch_lds_bytes(c->N) <= c->max_lds_per_block;
+  const char* sketch = !vec_shape ? "general" : (fused ? "fused" : "per_worker+reduce");
+  int radix = 0;
+  for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
+  std::snprintf(buf, static_cast<size_t>(len),
+                "sketch=%s rows_vectorised=%lld rows_general=%lld fused_lds_bytes=%zu "
+                "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld",
+                sketch, static_cast<long long>(vec_shape ? c->m_full : 0),
+                static_cast<long long>(vec_shape ? c->m - c->m_full : c->m),
+                arc::fused_sketch_lds_bytes(c->N), c->max_lds_per_block, c->buckets.size(),
+                radix, c->blocks.size(), static_cast<long long>(c->K_total));
   return ARC_OK;
 }
 

@@ -1,0 +1,52 @@
+// Device helpers shared by the libarctopk kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace arc {
+
+constexpr int kWave = 64;
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Load of data the kernel reads exactly once, marked non-temporal so that it
+// does not displace reusable lines.  Only for full 16-byte accesses: a
+// partial-line non-temporal load loses the rest of the line.
+__device__ __forceinline__ float4 stream_load(const float4* p) {
+  const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
+// bf16 halves of a 32-bit word, widened exactly to binary32.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Order this wave's LDS accesses: everything issued before has completed
+// before anything after is issued (LDS rows that only this wave touches).
+__device__ __forceinline__ void wave_lds_fence() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t o = __shfl_up(v, off, kWave);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+inline unsigned blocks_for(int64_t work, int threads) {
+  return (unsigned)((work + threads - 1) / threads);
+}
+
+}  // namespace arc

@@ -1,0 +1,320 @@
+// Top-K row selection of the compressor step (Eq. (4): I = arg top_K(Sigma)),
+// independently per bucket, with ties going to the lower row and the rows of
+// each bucket returned in ascending order.
+//
+// Radix select on the binary32 bit patterns of Sigma >= +0 (their unsigned
+// order is the numeric order), digits [31:21], [20:10], [9:0]:
+//   pass 0..2  each block histograms, in LDS, the digit of the keys that share
+//              the digits already fixed and adds its non-zero bins to the
+//              bucket's global histogram of that pass (integer atomics);
+//   pass p > 0 first fixes digit p-1: every block of the bucket walks the
+//              previous histogram from the top bin down to the bin holding the
+//              kleft-th largest remaining key (all blocks reach the same
+//              answer; the bucket's first block records it for the next
+//              kernel);
+//   count      fixes the last digit (the threshold key T and how many keys
+//              equal to T are kept) and counts, per block, keys above and equal
+//              to T;
+//   write      each block adds up the counts of the blocks before it, ranks
+//              its ties by row, writes the selected rows in order with
+//              block-wide prefix sums, and clears the histograms for the next
+//              step.
+// No kernel waits on another block: there are no grid-wide counters, and the
+// result does not depend on scheduling.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "arc_device.h"
+#include "arc_internal.h"
+
+namespace arc {
+namespace {
+
+template <int PASS>
+struct RadixDigit {
+  static constexpr int kShift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
+  static constexpr int kBits = PASS == 2 ? 10 : 11;
+  static constexpr uint32_t kMask = (1u << kBits) - 1u;
+  static constexpr int kBins = 1 << kBits;
+};
+
+constexpr int kKeysPerBatch = 8;
+
+__device__ __forceinline__ const uint32_t* hist_of(const SelectWorkspace& ws,
+                                                   int pass, int32_t b) {
+  return ws.hist + ((int64_t)pass * ws.nb + b) * kRadixBins;
+}
+__device__ __forceinline__ uint32_t* hist_of_mut(const SelectWorkspace& ws,
+                                                 int pass, int32_t b) {
+  return ws.hist + ((int64_t)pass * ws.nb + b) * kRadixBins;
+}
+
+// Executed by one full wave: append digit PASS to st using the bucket's
+// histogram of that pass.
+template <int PASS>
+__device__ BucketState fix_digit(const uint32_t* gh, BucketState st) {
+  using D = RadixDigit<PASS>;
+  constexpr int kPerLane = D::kBins / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  // lane 0 owns the top kPerLane bins, lane 1 the next ones, ...
+  const int top = D::kBins - 1 - lane * kPerLane;
+  uint32_t cnt[kPerLane];
+  uint32_t lane_sum = 0;
+#pragma unroll
+  for (int u = 0; u < kPerLane; ++u) {
+    cnt[u] = gh[top - u];
+    lane_sum += cnt[u];
+  }
+  const uint32_t incl = wave_inclusive_scan(lane_sum);
+  const uint32_t excl = incl - lane_sum;
+  const uint64_t kleft = (uint64_t)st.kleft;
+  const bool mine = (uint64_t)excl < kleft && kleft <= (uint64_t)incl;
+  const uint64_t who = __ballot(mine);
+  const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
+  uint32_t digit = 0, above = 0;
+  if (mine) {
+    uint32_t cum = excl;
+#pragma unroll
+    for (int u = 0; u < kPerLane; ++u) {
+      if ((uint64_t)cum + cnt[u] >= kleft) {
+        digit = (uint32_t)(top - u);
+        above = cum;
+        break;
+      }
+      cum += cnt[u];
+    }
+  }
+  digit = __shfl(digit, src, kWave);
+  above = __shfl(above, src, kWave);
+  st.prefix |= digit << D::kShift;
+  st.mask |= D::kMask << D::kShift;
+  st.kleft = (int64_t)(kleft - above);
+  return st;
+}
+
+// Radix state entering pass PASS (digits 0..PASS-1 fixed), computed by wave 0
+// and shared with the block.  The bucket's first block stores it.
+template <int PASS>
+__device__ BucketState state_before_pass(const SelectWorkspace& ws,
+                                         const BucketDesc& bk, int32_t b) {
+  __shared__ BucketState sh;
+  if (threadIdx.x < kWave) {
+    BucketState st;
+    if constexpr (PASS <= 1) {
+      st.prefix = 0u;
+      st.mask = 0u;
+      st.kleft = bk.k;
+    } else {
+      st = ws.state[b];
+    }
+    if constexpr (PASS >= 1) st = fix_digit<PASS - 1>(hist_of(ws, PASS - 1, b), st);
+    if (threadIdx.x == 0) {
+      sh = st;
+      if (PASS >= 1 && (int32_t)blockIdx.x == bk.first_blk) ws.state[b] = st;
+    }
+  }
+  __syncthreads();
+  return sh;
+}
+
+template <int PASS>
+__global__ void __launch_bounds__(kSelectThreads)
+radix_pass_kernel(const float* __restrict__ sigma, SelectWorkspace ws) {
+  using D = RadixDigit<PASS>;
+  __shared__ uint32_t lhist[kRadixBins];
+  const BlockDesc bd = ws.blocks[blockIdx.x];
+  const BucketDesc bk = ws.buckets[bd.bucket];
+  if (bk.mode != kSelectRadix) return;  // whole block
+  for (int b = threadIdx.x; b < D::kBins; b += kSelectThreads) lhist[b] = 0u;
+  const BucketState st = state_before_pass<PASS>(ws, bk, bd.bucket);  // syncs
+  for (int64_t base = bd.lo; base < bd.hi; base += kSelectThreads * kKeysPerBatch) {
+    uint32_t keys[kKeysPerBatch];
+    bool valid[kKeysPerBatch];
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      const int64_t p = base + u * kSelectThreads + threadIdx.x;
+      valid[u] = p < bd.hi;
+      keys[u] = valid[u] ? __float_as_uint(sigma[p]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u)
+      if (valid[u] && (keys[u] & st.mask) == st.prefix)
+        atomicAdd(&lhist[(keys[u] >> D::kShift) & D::kMask], 1u);
+  }
+  __syncthreads();
+  uint32_t* gh = hist_of_mut(ws, PASS, bd.bucket);
+  for (int b = threadIdx.x; b < D::kBins; b += kSelectThreads) {
+    const uint32_t c = lhist[b];
+    if (c != 0u) atomicAdd(&gh[b], c);
+  }
+}
+
+__global__ void __launch_bounds__(kSelectThreads)
+select_count_kernel(const float* __restrict__ sigma, SelectWorkspace ws) {
+  __shared__ uint32_t part[2][kSelectThreads / kWave];
+  const BlockDesc bd = ws.blocks[blockIdx.x];
+  const BucketDesc bk = ws.buckets[bd.bucket];
+  if (bk.mode != kSelectRadix) return;  // whole block
+  const BucketState st = state_before_pass<3>(ws, bk, bd.bucket);  // syncs
+  const uint32_t T = st.prefix;
+  uint32_t gt = 0, eq = 0;
+  for (int64_t base = bd.lo; base < bd.hi; base += kSelectThreads * kKeysPerBatch) {
+    uint32_t keys[kKeysPerBatch];
+    bool valid[kKeysPerBatch];
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      const int64_t p = base + u * kSelectThreads + threadIdx.x;
+      valid[u] = p < bd.hi;
+      keys[u] = valid[u] ? __float_as_uint(sigma[p]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      gt += valid[u] && keys[u] > T;
+      eq += valid[u] && keys[u] == T;
+    }
+  }
+  gt = wave_sum(gt);
+  eq = wave_sum(eq);
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    part[0][wave] = gt;
+    part[1][wave] = eq;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t tg = 0, te = 0;
+    for (int w = 0; w < kSelectThreads / kWave; ++w) {
+      tg += part[0][w];
+      te += part[1][w];
+    }
+    ws.blockcnt[2 * blockIdx.x] = tg;
+    ws.blockcnt[2 * blockIdx.x + 1] = te;
+  }
+}
+
+// Exclusive prefix sum over the block (blockDim.x == kSelectThreads).
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v) {
+  __shared__ uint32_t wsum[kSelectThreads / kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const uint32_t incl = wave_inclusive_scan(v);
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0;
+#pragma unroll
+  for (int w = 0; w < kSelectThreads / kWave; ++w)
+    if (w < wave) before += wsum[w];
+  __syncthreads();
+  return before + incl - v;
+}
+
+__global__ void __launch_bounds__(kSelectThreads)
+select_write_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
+                    int32_t* __restrict__ out_idx) {
+  __shared__ uint32_t sh_before[2];
+  const BlockDesc bd = ws.blocks[blockIdx.x];
+  const BucketDesc bk = ws.buckets[bd.bucket];
+  if (bk.mode == kSelectNone) return;  // whole block
+  if (bk.mode == kSelectAll) {
+    for (int64_t p = bd.lo + threadIdx.x; p < bd.hi; p += kSelectThreads)
+      out_idx[bk.out_off + (p - bk.lo)] = (int32_t)p;
+    return;
+  }
+  const BucketState st = ws.state[bd.bucket];
+  const uint32_t T = st.prefix;
+  const uint64_t kleft = (uint64_t)st.kleft;
+  // Keys above / equal to T in the bucket's earlier blocks.
+  if (threadIdx.x < kWave) {
+    uint32_t g_before = 0, e_before = 0;
+    for (int32_t j = bk.first_blk + (int32_t)threadIdx.x; j < (int32_t)blockIdx.x; j += kWave) {
+      g_before += ws.blockcnt[2 * j];
+      e_before += ws.blockcnt[2 * j + 1];
+    }
+    g_before = wave_sum(g_before);
+    e_before = wave_sum(e_before);
+    if (threadIdx.x == 0) {
+      sh_before[0] = g_before;
+      sh_before[1] = e_before;
+    }
+  }
+  // This block's share of clearing the bucket's three histograms.
+  {
+    const int32_t jb = (int32_t)blockIdx.x - bk.first_blk;
+    const int64_t total = (int64_t)kRadixPasses * kRadixBins;
+    for (int64_t e = (int64_t)jb * kSelectThreads + threadIdx.x; e < total;
+         e += (int64_t)bk.nblk * kSelectThreads)
+      hist_of_mut(ws, (int)(e / kRadixBins), bd.bucket)[e % kRadixBins] = 0u;
+  }
+  __syncthreads();
+  const uint32_t gt_block = sh_before[0], eq_block = sh_before[1];
+  // Thread t owns rows [r0, r1), contiguous, so block order is row order.
+  const int64_t r0 = bd.lo + (int64_t)threadIdx.x * bk.rows_per_thread;
+  const int64_t r1 = r0 + bk.rows_per_thread < bd.hi ? r0 + bk.rows_per_thread : bd.hi;
+  uint32_t n_eq = 0, n_gt = 0;
+  for (int64_t b = r0; b < r1; b += kKeysPerBatch) {
+    uint32_t keys[kKeysPerBatch];
+    bool valid[kKeysPerBatch];
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      valid[u] = b + u < r1;
+      keys[u] = valid[u] ? __float_as_uint(sigma[b + u]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      n_gt += valid[u] && keys[u] > T;
+      n_eq += valid[u] && keys[u] == T;
+    }
+  }
+  const uint64_t eq_rank0 = (uint64_t)eq_block + block_exclusive_scan(n_eq);
+  // ties this thread keeps: ranks eq_rank0 .. eq_rank0 + n_eq - 1 below kleft
+  const uint64_t ties_kept =
+      eq_rank0 >= kleft ? 0 : ((kleft - eq_rank0) < n_eq ? (kleft - eq_rank0) : n_eq);
+  const uint32_t n_sel = n_gt + (uint32_t)ties_kept;
+  const uint64_t taken_before = (uint64_t)eq_block < kleft ? eq_block : kleft;
+  int64_t pos = bk.out_off + (int64_t)gt_block + (int64_t)taken_before +
+                block_exclusive_scan(n_sel);
+  const int64_t end = bk.out_off + bk.k;
+  uint64_t rank = eq_rank0;
+  for (int64_t b = r0; b < r1; b += kKeysPerBatch) {
+    uint32_t keys[kKeysPerBatch];
+    bool valid[kKeysPerBatch];
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      valid[u] = b + u < r1;
+      keys[u] = valid[u] ? __float_as_uint(sigma[b + u]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      bool sel = false;
+      if (valid[u]) {
+        if (keys[u] > T) {
+          sel = true;
+        } else if (keys[u] == T) {
+          sel = rank < kleft;
+          ++rank;
+        }
+      }
+      // pos stays below the bucket's end by construction; the bound keeps a
+      // broken invariant from writing outside out_idx.
+      if (sel && pos < end) out_idx[pos++] = (int32_t)(b + u);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* sigma, const SelectWorkspace& ws,
+                         int32_t* out_idx, hipStream_t stream) {
+  const dim3 grid((unsigned)ws.nblk), block(kSelectThreads);
+  if (ws.any_radix) {
+    hipLaunchKernelGGL(radix_pass_kernel<0>, grid, block, 0, stream, sigma, ws);
+    hipLaunchKernelGGL(radix_pass_kernel<1>, grid, block, 0, stream, sigma, ws);
+    hipLaunchKernelGGL(radix_pass_kernel<2>, grid, block, 0, stream, sigma, ws);
+    hipLaunchKernelGGL(select_count_kernel, grid, block, 0, stream, sigma, ws);
+  }
+  if (ws.any_output)
+    hipLaunchKernelGGL(select_write_kernel, grid, block, 0, stream, sigma, ws, out_idx);
+  return hipGetLastError();
+}
+
+}  // namespace arc

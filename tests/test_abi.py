@@ -96,6 +96,7 @@ def test_null_context_paths():
         assert getattr(L, fn)(None, None) == arc.ARC_ERR_INVALID
     assert L.arc_timing_enable(None, 1) == arc.ARC_ERR_INVALID
     assert L.arc_debug_projection(None, 0, None) == arc.ARC_ERR_INVALID
+    assert L.arc_describe(None, None, 0) == arc.ARC_ERR_INVALID
     assert L.arc_timing_read(None, None, None) == arc.ARC_ERR_INVALID
 
 

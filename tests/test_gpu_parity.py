@@ -42,6 +42,8 @@ CASES = [
     ("eta_one", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=1.0, steps=2)),
     ("eta_zero", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=0.0, steps=2)),
     ("select_multiblock", dict(d=32 * 9000, N=2, n=32, r=4, K=2500, steps=2)),
+    ("per_worker_N12", dict(d=256 * 300, N=12, n=256, r=4, K=7, steps=2)),
+    ("select_many_blocks", dict(d=32 * 300_000, N=1, n=32, r=4, K=150_000, steps=1)),
 ]
 
 
@@ -49,6 +51,22 @@ CASES = [
 def test_parity_small(name, kw):
     log(f"[parity] {name} {kw}")
     run_case(label=name, check_S=True, **kw)
+
+
+def test_describe_names_the_kernel_path():
+    for N, want in ((4, "sketch=fused"), (8, "sketch=fused"), (12, "sketch=per_worker+reduce")):
+        comp = arc.Compressor(d=256 * 64, N=N, n=256, K=3, eta=0.1, seed=1)
+        try:
+            desc = comp.describe()
+            log(f"[describe] N={N}: {desc}")
+            assert want in desc, desc
+        finally:
+            comp.close()
+    comp = arc.Compressor(d=100 * 64, N=2, n=100, r=3, K=3, eta=0.1, seed=1)
+    try:
+        assert "sketch=general" in comp.describe()
+    finally:
+        comp.close()
 
 
 def test_parity_misaligned_pointers_take_the_general_path():
