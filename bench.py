@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
 DEFAULT_WORKLOAD = "llama1b"    # the 1.1B-parameter configuration
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sketch_traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2510_26709_amd", "csrc", "arc_kernels.hip")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2510_26709_amd", "csrc", "arc_sketch.hip")
 
 
 def log(msg):
@@ -50,16 +50,28 @@ def algorithmic_bytes(w, K_total):
             select + gather + 4 * K_total}
 
 
+def kernel_source_digest(path=KERNEL_SOURCE):
+    """sha256 of the kernel source with comments and whitespace removed, so
+    that the recorded counters stay valid across comment-only edits."""
+    import re
+    with open(path) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = re.sub(r"\s+", "", src)
+    return hashlib.sha256(src.encode()).hexdigest()
+
+
 def kernel_traffic(w):
     """HBM bytes per launch of the sketch kernel from committed rocprofv3
-    counters, if they were taken on the current kernel source."""
+    counters (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads
+    for a plain copy of known size), if they were taken on the current kernel
+    source; otherwise None."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-        with open(KERNEL_SOURCE, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
         entry = rec.get("workloads", {}).get(w.name)
-        if rec.get("kernel_source_sha256") != sha or entry is None:
+        if rec.get("kernel_source_digest") != kernel_source_digest() or entry is None:
             return None
         return float(entry["hbm_bytes_per_launch"])
     except (OSError, ValueError, KeyError):
@@ -132,15 +144,20 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--batches", type=int, default=4,
                     help="distinct gradient batches kept resident and cycled")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--print-kernel-digest", action="store_true",
+                    help="print the digest of the sketch kernel source and exit")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="instead of the compressor, time a plain device copy of GIB "
                          "gibibytes (empirical bandwidth ceiling; counter calibration)")
     args = ap.parse_args()
+    if args.print_kernel_digest:
+        print(kernel_source_digest())
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one MI355X: the compressor path here is single-GPU "
               "(workers are simulated on the device); run with --gpus 1.", file=sys.stderr)
@@ -235,7 +252,8 @@ def main():
         "path": comp_desc,
         "roofline": {
             "bound": "hbm",
-            "kernel": "sketch_fast_kernel (momentum + residual + per-worker sketch)",
+            "kernel": "sketch_fused_kernel (momentum + residual + sketch + worker sum + "
+                      "importance)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

@@ -43,6 +43,12 @@ CASES = [
     ("eta_zero", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=0.0, steps=2)),
     ("select_multiblock", dict(d=32 * 9000, N=2, n=32, r=4, K=2500, steps=2)),
     ("per_worker_N12", dict(d=256 * 300, N=12, n=256, r=4, K=7, steps=2)),
+    ("bf16_odd_chunks", dict(d=96 * 700 + 12, N=3, n=96, r=4, K=9, steps=2, grad_dtype="bf16",
+                             family=1)),
+    ("bf16_per_worker_N9", dict(d=128 * 500, N=9, n=128, r=4, K=6, steps=2, grad_dtype="bf16",
+                                family=1)),
+    ("bf16_fused_r8_N2", dict(d=64 * 3000, N=2, n=64, r=8, K=40, steps=2, grad_dtype="bf16",
+                              family=1)),
     ("select_many_blocks", dict(d=32 * 300_000, N=1, n=32, r=4, K=150_000, steps=1)),
 ]
 
