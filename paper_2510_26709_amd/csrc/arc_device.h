@@ -18,6 +18,21 @@ __device__ __forceinline__ float4 stream_load(const float4* p) {
   return make_float4(v.x, v.y, v.z, v.w);
 }
 
+// Store of data nobody reads again in this kernel, marked non-temporal.
+__device__ __forceinline__ void stream_store(float4* p, float4 v) {
+  const f32x4_t w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<f32x4_t*>(p));
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs of the MI355X (block
+// b starts on XCD b % 8).  This bijection of [0, nblocks) hands each XCD one
+// contiguous range of blocks (the last nblocks % 8 map to themselves).
+__device__ __forceinline__ int64_t xcd_contiguous_block(int64_t b, int64_t nblocks) {
+  constexpr int64_t kXcds = 8;
+  const int64_t per = nblocks / kXcds;
+  return b < per * kXcds ? (b % kXcds) * per + b / kXcds : b;
+}
+
 // bf16 halves of a 32-bit word, widened exactly to binary32.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }

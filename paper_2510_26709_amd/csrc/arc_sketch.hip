@@ -77,7 +77,7 @@ __device__ __forceinline__ void sketch_rows_impl(
       hn.z = fmaf(eta, xv[u].z, a * hv[u].z);
       hn.w = fmaf(eta, xv[u].w, a * hv[u].w);
       const int64_t p = p0 + u * 8 + sub;
-      if (FULL || p < row_hi) *reinterpret_cast<float4*>(h + wbase + p * n + col) = hn;
+      if (FULL || p < row_hi) stream_store(reinterpret_cast<float4*>(h + wbase + p * n + col), hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
@@ -132,7 +132,7 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
   extern __shared__ float4 lds_tiles[];  // N tiles of kTileF4
   const int lane = threadIdx.x & (kWave - 1);
   const int i = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // worker
-  const int64_t p0 = row_lo + (int64_t)blockIdx.x * kWave;
+  const int64_t p0 = row_lo + xcd_contiguous_block(blockIdx.x, gridDim.x) * kWave;
   float4* tile = lds_tiles + i * kTileF4;
   float s[R];
   sketch_rows<R, BF16>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tile, s);
@@ -176,7 +176,8 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t i = blockIdx.y;
-  const int64_t p0 = row_lo + ((int64_t)blockIdx.x * kSketchWaves + wave) * kWave;
+  const int64_t p0 =
+      row_lo + (xcd_contiguous_block(blockIdx.x, gridDim.x) * kSketchWaves + wave) * kWave;
   if (p0 >= row_hi) return;  // whole wave; no block barrier follows
   float s[R];
   sketch_rows<R, BF16>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tiles[wave], s);
