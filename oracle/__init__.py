@@ -41,6 +41,9 @@ def _load():
         "oracle_step": (ctypes.c_int, [_i32, _i64, _i64, _i32, _f32, _u64, _i64, _i64, _i32,
                                        _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _vp, _vp]),
+        "oracle_step_tensors": (ctypes.c_int, [_i32, _i32, _f32, _u64, _i64, _i32, _vp, _vp, _vp,
+                                               _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                               _vp]),
         "oracle_num_threads": (ctypes.c_int, []),
     }
     for name, (res, args) in sig.items():
@@ -203,6 +206,43 @@ def step(h: np.ndarray, g: np.ndarray, grad: np.ndarray, *, n: int, r: int, eta:
                                _ptr(S)), "step")
     k = total.value
     out = {"idx": idx[:k].copy(), "agg": agg[:k].copy()}
+    if want_sigma:
+        out["sigma"] = sigma
+    if want_S:
+        out["S"] = S
+    return out
+
+
+def step_tensors(h: np.ndarray, g: np.ndarray, grad: np.ndarray, tensors, *, r: int, eta: float,
+                 seed: int, t: int, want_sigma: bool = False, want_S: bool = False) -> dict:
+    """Per-tensor step; tensors = [(rows, cols, K), ...] laid out consecutively.
+
+    Returns {"idx": int32[K_total] (global rows), "agg": float32[agg_len] (packed
+    rows of each tensor's width)} plus "sigma" / "S" when asked for.
+    """
+    _f32c(h, "h"), _f32c(g, "g")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    N, d = h.shape
+    tens = np.asarray(tensors, dtype=np.int64).reshape(-1, 3)
+    rows = np.ascontiguousarray(tens[:, 0])
+    cols = np.ascontiguousarray(tens[:, 1])
+    ks = np.ascontiguousarray(tens[:, 2])
+    if int((rows * cols).sum()) != d or g.shape != h.shape or grad.shape != h.shape:
+        raise ValueError("tensors must cover d exactly; h, g, grad must be [N, d]")
+    m = int(rows.sum())
+    kept = np.minimum(np.maximum(ks, 0), rows)
+    idx = np.empty(max(int(kept.sum()), 1), dtype=np.int32)
+    agg = np.empty(max(int((kept * cols).sum()), 1), dtype=np.float32)
+    sigma = np.empty(m, dtype=np.float32) if want_sigma else None
+    S = np.empty((N, m, r), dtype=np.float32) if want_S else None
+    total = ctypes.c_int64(0)
+    alen = ctypes.c_int64(0)
+    _check(_load().oracle_step_tensors(N, r, eta, seed & (2**64 - 1), t, len(rows), _ptr(rows),
+                                       _ptr(cols), _ptr(ks), _ptr(grad), is_bf16, _ptr(h),
+                                       _ptr(g), _ptr(idx), _ptr(agg), ctypes.addressof(total),
+                                       ctypes.addressof(alen), _ptr(sigma), _ptr(S)),
+           "step_tensors")
+    out = {"idx": idx[: total.value].copy(), "agg": agg[: alen.value].copy()}
     if want_sigma:
         out["sigma"] = sigma
     if want_S:

@@ -340,3 +340,114 @@ done:
   if (!sigma_out) free(sigma);
   return rc;
 }
+
+/* ---------------------------------------------------------------------------
+ * Per-tensor mode (Sec. VI): the model's tensors are compressed one by one,
+ * each in its own m_b x n_b view (2-D weights as they are, convolution
+ * kernels as out x (in*kh*kw), 1-D tensors as one row kept whole), with its
+ * own K_b.  Per tensor, the step is Alg. 1 applied to Delta = h_t - g_{t-1}
+ * inside EF21M (11a), (11b), exactly as in oracle_step: the sketch with the
+ * projection of the tensor's width, the worker sum, the importance, the
+ * arg-top-K of the tensor's rows, and the gather/update of its selected
+ * rows.  Tensors of the same width share V_t (V depends on (seed, t, width)).
+ * Global row numbering: tensor b's rows follow tensor b-1's.
+ * ------------------------------------------------------------------------- */
+int oracle_step_tensors(int32_t N, int32_t r, float eta, uint64_t seed,
+                        int64_t t, int32_t num_tensors, const int64_t *rows,
+                        const int64_t *cols, const int64_t *K,
+                        const void *grad, int32_t grad_is_bf16, float *h,
+                        float *g, int32_t *idx, float *agg, int64_t *K_total,
+                        int64_t *agg_len, float *sigma_out, float *S_out) {
+  if (N < 1 || r < 1 || num_tensors < 1 || rows == NULL || cols == NULL ||
+      K == NULL || grad == NULL || h == NULL || g == NULL || idx == NULL ||
+      agg == NULL || K_total == NULL || agg_len == NULL)
+    return 1;
+  int64_t d = 0, m = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) {
+    if (rows[b] < 1 || cols[b] < 1 || K[b] < 0) return 1;
+    d += rows[b] * cols[b];
+    m += rows[b];
+  }
+  if (m > INT32_MAX) return 1;
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) return 1;
+
+  float *S = S_out ? S_out : (float *)malloc((size_t)((int64_t)N * m * r) * sizeof(float));
+  float *P = (float *)malloc((size_t)(m * r) * sizeof(float));
+  float *sigma = sigma_out ? sigma_out : (float *)malloc((size_t)m * sizeof(float));
+  int rc = 1;
+  if (S == NULL || P == NULL || sigma == NULL) goto done;
+
+  /* Sketch, tensor by tensor, each with the projection of its width. */
+  {
+    int64_t off = 0, row0 = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) {
+      const int64_t mb = rows[b], nb = cols[b];
+      float *V = (float *)malloc((size_t)(nb * r) * sizeof(float));
+      if (V == NULL || oracle_projection(seed, t, nb, r, V)) {
+        free(V);
+        goto done;
+      }
+#pragma omp parallel for schedule(static)
+      for (int64_t ip = 0; ip < (int64_t)N * mb; ++ip) {
+        const int64_t i = ip / mb, p = ip % mb;
+        const float *hi = h + i * d + off + p * nb, *gi = g + i * d + off + p * nb;
+        for (int32_t k = 0; k < r; ++k) {
+          float acc = 0.0f;
+          for (int64_t j = 0; j < nb; ++j) acc = fmaf(hi[j] - gi[j], V[j * r + k], acc);
+          S[((int64_t)i * m + row0 + p) * r + k] = acc;
+        }
+      }
+      free(V);
+      off += mb * nb;
+      row0 += mb;
+    }
+  }
+  if (oracle_worker_sum(N, m, r, S, P)) goto done;
+  if (oracle_importance(m, r, P, sigma)) goto done;
+
+  /* Arg-top-K per tensor: the tensors are the buckets of the selection. */
+  {
+    int64_t *begin = (int64_t *)malloc((size_t)(num_tensors + 1) * sizeof(int64_t));
+    if (begin == NULL) goto done;
+    begin[0] = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) begin[b + 1] = begin[b] + rows[b];
+    const int bad = oracle_select(m, sigma, 0, num_tensors, begin, K, idx, K_total);
+    free(begin);
+    if (bad) goto done;
+  }
+
+  /* Gather + worker sum + EF update, tensor by tensor, packed payload. */
+  {
+    int64_t off = 0, row0 = 0, q0 = 0, a0 = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) {
+      const int64_t mb = rows[b], nb = cols[b];
+      const int64_t kb = K[b] < mb ? K[b] : mb;
+#pragma omp parallel for schedule(static)
+      for (int64_t q = 0; q < kb; ++q) {
+        const int64_t p = idx[q0 + q] - row0;
+        for (int64_t j = 0; j < nb; ++j) {
+          const int64_t e = off + p * nb + j;
+          float acc = 0.0f;
+          for (int32_t i = 0; i < N; ++i) {
+            const int64_t at = (int64_t)i * d + e;
+            const float delta = h[at] - g[at];
+            acc = (i == 0) ? delta : acc + delta;
+            g[at] = g[at] + delta;
+          }
+          agg[a0 + q * nb + j] = acc;
+        }
+      }
+      off += mb * nb;
+      row0 += mb;
+      q0 += kb;
+      a0 += kb * nb;
+    }
+    *agg_len = a0;
+  }
+  rc = 0;
+done:
+  if (!S_out) free(S);
+  free(P);
+  if (!sigma_out) free(sigma);
+  return rc;
+}

@@ -83,6 +83,20 @@ int oracle_step(int32_t N, int64_t d, int64_t n, int32_t r, float eta,
                 float *agg, int64_t *K_total, const float *V_override,
                 float *sigma_out, float *S_out);
 
+/* Per-tensor mode (Sec. VI: each tensor of the model is compressed in its own
+ * 2-D view with its own K; 1-D tensors are kept whole).  Tensor b covers the
+ * rows[b]*cols[b] consecutive coordinates after tensor b-1 (sum = d), viewed
+ * row-major; its rows are global rows [row_b, row_b + rows[b]) of Sigma, S and
+ * idx.  V for a tensor of width w is oracle_projection(seed, t, w, r).  agg is
+ * packed: tensor b's K_b selected rows of cols[b] values follow tensor b-1's.
+ * *K_total and *agg_len receive the output sizes. */
+int oracle_step_tensors(int32_t N, int32_t r, float eta, uint64_t seed,
+                        int64_t t, int32_t num_tensors, const int64_t *rows,
+                        const int64_t *cols, const int64_t *K,
+                        const void *grad, int32_t grad_is_bf16, float *h,
+                        float *g, int32_t *idx, float *agg, int64_t *K_total,
+                        int64_t *agg_len, float *sigma_out, float *S_out);
+
 /* Number of threads the oracle's parallel loops use. */
 int oracle_num_threads(void);
 
