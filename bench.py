@@ -45,7 +45,7 @@ def algorithmic_bytes(w, K_total):
     sketch_out = 4 * w.N * w.m * w.r                # per-worker sketch written
     reduce_ = 4 * w.N * w.m * w.r + 4 * w.m         # sketch read, importance written
     select = 4 * 4 * w.m                            # importance read by 4 passes
-    gather = K_total * w.n * (12 * w.N + 4)         # h, g read, g written, agg written
+    gather = w.payload_elems() * (12 * w.N + 4)     # h, g read, g written, agg written
     return {"sketch_kernel": stream + sketch_out, "step": stream + sketch_out + reduce_ +
             select + gather + 4 * K_total}
 
@@ -78,18 +78,37 @@ def kernel_traffic(w):
         return None
 
 
+def _prefix(w, elems):
+    """A prefix of the workload of about `elems` coordinates per worker, as
+    (d_s, oracle step keyword arguments, description): whole rows of the
+    single view with K scaled to the same ratio, or whole tensors with their
+    own K."""
+    if not w.per_tensor:
+        rows = max(1, min(w.m, elems // w.n))
+        K_s = max(1, math.ceil(w.mu * rows))
+        return rows * w.n, dict(n=w.n, K=K_s), f"first {rows} of {w.m} rows (n={w.n}, K={K_s})"
+    views = w.tensor_views()
+    take, d_s = [], 0
+    for v in views:
+        if take and d_s + v[0] * v[1] > elems:
+            break
+        take.append(v)
+        d_s += v[0] * v[1]
+    K_s = sum(min(k, r) for r, _, k in take)
+    return d_s, dict(tensors=take), f"first {len(take)} of {len(views)} tensors (K={K_s} rows)"
+
+
 def cpu_baseline(w, grads_dev, seconds_target=12.0):
-    """Time the CPU oracle on a prefix of the workload: the first m_s rows of
-    every worker's vector (d_s = m_s * n), K scaled to the same ratio, from
-    h = g = 0, on the same synthetic gradients (copied from the device)."""
+    """Time the CPU oracle on a prefix of the workload (the first coordinates
+    of every worker's vector, whole rows or whole tensors) from h = g = 0, on
+    the same synthetic gradients (copied from the device)."""
     import numpy as np
 
     import oracle
     threads = oracle.num_threads()
 
-    def run(rows, steps):
-        d_s = rows * w.n
-        K_s = max(1, math.ceil(w.mu * rows))
+    def run(elems, steps):
+        d_s, kw, desc = _prefix(w, elems)
         h = np.zeros((w.N, d_s), np.float32)
         g = np.zeros((w.N, d_s), np.float32)
         grads = []
@@ -98,25 +117,28 @@ def cpu_baseline(w, grads_dev, seconds_target=12.0):
             grads.append(gd.view(np.uint16) if w.grad_dtype == "bf16" else gd)
         t0 = time.perf_counter()
         for s in range(steps):
-            oracle.step(h, g, grads[s], n=w.n, r=w.r, eta=w.eta, seed=w.sketch_seed, t=s, K=K_s)
-        return (time.perf_counter() - t0) / steps, d_s, K_s
+            if w.per_tensor:
+                oracle.step_tensors(h, g, grads[s], kw["tensors"], r=w.r, eta=w.eta,
+                                    seed=w.sketch_seed, t=s)
+            else:
+                oracle.step(h, g, grads[s], r=w.r, eta=w.eta, seed=w.sketch_seed, t=s, **kw)
+        return (time.perf_counter() - t0) / steps, d_s, desc
 
     # calibrate on a small prefix, then size the sample to the time target
-    rows0 = max(1, min(w.m, (1 << 22) // w.n))
-    t1, _, _ = run(rows0, 1)
-    per_row = t1 / rows0
+    t1, d1, _ = run(1 << 22, 1)
+    per_elem = t1 / d1
     steps = 2
-    rows = int(min(w.m, max(rows0, seconds_target / steps / max(per_row, 1e-12))))
-    if rows == w.m:  # whole workload fits the time budget: spend it on more steps
-        steps = int(max(2, min(8, seconds_target / max(per_row * rows, 1e-9))))
-    t_step, d_s, K_s = run(rows, steps)
+    elems = int(min(w.d, max(d1, seconds_target / steps / max(per_elem, 1e-15))))
+    if elems >= w.d:  # whole workload fits the time budget: spend it on more steps
+        steps = int(max(2, min(8, seconds_target / max(per_elem * w.d, 1e-9))))
+    t_step, d_s, desc = run(elems, steps)
     return {
         "value": w.N * d_s / t_step,
         "unit": "gradient elements/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"first {rows} of {w.m} rows per worker (d={d_s}, N={w.N}, n={w.n}, "
-                   f"K={K_s} rows), {steps} steps from h=g=0, mean s/step={t_step:.3f}"),
+        "sample": (f"{desc} per worker: d={d_s} of {w.d}, N={w.N}; {steps} steps from h=g=0, "
+                   f"mean s/step={t_step:.3f}"),
     }
 
 
@@ -191,7 +213,9 @@ def main():
         g = torch.zeros((w.N, w.d), dtype=torch.float32, device=dev)
         comp = arc.Compressor(d=w.d, N=w.N, n=w.n, r=w.r, K=w.K_global(), eta=w.eta,
                               seed=w.sketch_seed, grad_dtype=w.grad_dtype,
-                              buckets=w.buckets(), device=dev, stream=stream)
+                              buckets=w.buckets(),
+                              tensors=w.tensor_views() if w.per_tensor else None,
+                              device=dev, stream=stream)
         stream.synchronize()
         log(f"[bench] m={comp.m} K_total={comp.K_total}; {comp.describe()}; warmup {args.warmup}")
         for t in range(args.warmup):
@@ -245,15 +269,19 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "d": w.d, "N": w.N, "n": w.n, "r": w.r, "m": comp.m,
                    "K_rows": comp.K_total, "grad_dtype": w.grad_dtype, "eta": w.eta,
-                   "mu": w.mu, "buckets": 0 if w.buckets() is None else len(w.buckets()[1])},
+                   "mu": w.mu, "buckets": 0 if w.buckets() is None else len(w.buckets()[1]),
+                   "view": "per_tensor" if w.per_tensor else "single",
+                   "tensors": len(w.views) if w.per_tensor else 0,
+                   "payload_elems": comp.payload},
         "step_hbm_GBps": step_gbps,
         "step_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "stage_ms": stages,
         "path": comp_desc,
         "roofline": {
             "bound": "hbm",
-            "kernel": "sketch_fused_kernel (momentum + residual + sketch + worker sum + "
-                      "importance)",
+            "kernel": "sketch stage: sketch_fused_kernel launches (momentum + residual + "
+                      "sketch + worker sum + importance), plus the general-row kernels "
+                      "where the layout has any",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

@@ -71,6 +71,18 @@ typedef enum { ARC_DTYPE_F32 = 0, ARC_DTYPE_BF16 = 1 } arc_dtype;
 #define ARC_MAX_R 32
 
 /*
+ * One tensor of the per-tensor mode: `rows` x `cols` consecutive coordinates
+ * viewed row-major, compressed with its own K (Sec. VI: each 2-D tensor in
+ * its own view, convolution kernels as out x (in*kh*kw), 1-D tensors kept
+ * whole, e.g. as one row with K = 1).
+ */
+typedef struct {
+  int64_t rows; /* >= 1 */
+  int64_t cols; /* >= 1 */
+  int64_t K;    /* rows kept, >= 0; K >= rows keeps the tensor whole */
+} arc_tensor;
+
+/*
  * Problem description (Alg. 1 inputs, EF21M step size, shared seed).
  *   d            coordinates per worker (> 0)
  *   n            row width of the m x n view (> 0); m = ceil(d/n) <= 2^31-1
@@ -89,6 +101,14 @@ typedef enum { ARC_DTYPE_F32 = 0, ARC_DTYPE_BF16 = 1 } arc_dtype;
  *   grad_dtype   arc_dtype of the gradients; h and g are always binary32
  *   num_buckets  0 for one global selection over all m rows
  *   eta          EF21M momentum weight, 0 <= eta <= 1
+ *   tensors, num_tensors
+ *                per-tensor mode (num_tensors > 0): the d coordinates are
+ *                tensors[0], tensors[1], ... in order (sum of rows*cols ==
+ *                d); each tensor is its own m_b x n_b view with its own K_b,
+ *                the global rows are tensor 0's rows, then tensor 1's, ...;
+ *                n, K and num_buckets must then be 0.  A tensor of width w
+ *                uses the projection V_t of width w (tensors of equal width
+ *                share it).  Host array, copied by arc_create.
  */
 typedef struct {
   int64_t d;
@@ -103,6 +123,9 @@ typedef struct {
   int32_t num_buckets;
   float eta;
   int32_t reserved; /* must be 0 */
+  const arc_tensor *tensors;
+  int32_t num_tensors;
+  int32_t reserved2; /* must be 0 */
 } arc_config;
 
 /*
@@ -122,12 +145,14 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  *            (Eq. (11b)), all other elements are left bit-for-bit unchanged
  *   out_idx  [K_total] int32: the selected rows, ascending within each bucket,
  *            buckets in order
- *   out_agg  [K_total*n] binary32: row q holds sum_i Delta^(i) of row
- *            out_idx[q] (ascending worker order); +0 past d
+ *   out_agg  [arc_payload_elems(ctx)] binary32: the selected rows in
+ *            out_idx order, each as sum_i Delta^(i) of that row (ascending
+ *            worker order).  Single view: K_total rows of n values, +0 past
+ *            d.  Per-tensor mode: packed, each row with its tensor's width.
  * K_total = arc_selected_rows(ctx).  out_idx / out_agg may be NULL only when
- * K_total == 0.  Pointers 16-byte aligned with d % 4 == 0 and n % 32 == 0
- * take the vectorised path; anything else takes a slower path with identical
- * results.
+ * K_total == 0.  Pointers 16-byte aligned with d % 4 == 0 and row widths
+ * that are multiples of 32 take the vectorised path; anything else takes a
+ * slower path with identical results.
  */
 arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
                     float *g, int32_t *out_idx, float *out_agg);
@@ -141,6 +166,15 @@ int64_t arc_num_rows(const arc_ctx *ctx);
 
 /* Rows selected per step after clamping each K to its bucket; -1 for NULL. */
 int64_t arc_selected_rows(const arc_ctx *ctx);
+
+/* Elements of out_agg per step; -1 for NULL. */
+int64_t arc_payload_elems(const arc_ctx *ctx);
+
+/* V_t of width n (n x r binary32, row-major) for a shared seed, written to
+ * host memory V: the projection every step of that seed uses for rows of
+ * width n.  Host only; needs no device. */
+arc_status arc_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
+                          float *V);
 
 /* Static string naming a status code. */
 const char *arc_status_str(arc_status s);
@@ -165,11 +199,13 @@ arc_status arc_debug_sigma(arc_ctx *ctx, float *out_sigma);
 arc_status arc_debug_sketch(arc_ctx *ctx, float *out_S);
 
 /* Write V_t ([n][r] binary32, row-major) for step t into host memory out_V,
- * exactly as arc_step would use it (honours arc_set_projection). */
+ * exactly as arc_step would use it (honours arc_set_projection).  Single-view
+ * mode only; in per-tensor mode use arc_projection with the tensor's width. */
 arc_status arc_debug_projection(arc_ctx *ctx, int64_t t, float *out_V);
 
 /* Use the host matrix V ([n][r] binary32, copied) for every later step
- * instead of V_t; NULL restores the seeded projection. */
+ * instead of V_t; NULL restores the seeded projection.  Single-view mode
+ * only (ARC_ERR_UNSUPPORTED in per-tensor mode). */
 arc_status arc_set_projection(arc_ctx *ctx, const float *V);
 
 /* Stage timing: when enabled, arc_step records HIP events on the context's

@@ -11,38 +11,45 @@ from ._lib import (  # noqa: F401
     ARC_DTYPE_BF16, ARC_DTYPE_F32, ARC_ERR_DEVICE, ARC_ERR_INVALID, ARC_ERR_NOMEM,
     ARC_ERR_UNSUPPORTED, ARC_MAX_R, ARC_NUM_STAGES, ARC_OK, EXPORTED, LIB_PATH, STAGE_NAMES,
     ArcError, arc_config, arc_create, arc_debug_projection, arc_describe, arc_debug_sigma, arc_debug_sketch,
-    arc_destroy, arc_last_error, arc_num_rows, arc_selected_rows, arc_set_projection,
-    arc_status_str, arc_step, arc_timing_enable, arc_timing_read, make_config)
+    arc_destroy, arc_last_error, arc_num_rows, arc_payload_elems, arc_projection,
+    arc_selected_rows, arc_set_projection, arc_status_str, arc_step, arc_tensor,
+    arc_timing_enable, arc_timing_read, make_config)
 
 
 class Compressor:
     """One libarctopk context bound to a torch stream, with its outputs.
 
     ``step(t, grad, h, g)`` enqueues one compressor step and returns the
-    device tensors (idx [K_total] int32, agg [K_total, n] float32); they are
-    overwritten by the next step.
+    device tensors idx [K_total] int32 and agg, overwritten by the next step:
+    [K_total, n] float32 for one m x n view, or, with ``tensors`` =
+    [(rows, cols, K), ...] (per-tensor mode), the packed 1-D payload.
     """
 
-    def __init__(self, *, d, N, n, r=4, K=0, eta, seed, grad_dtype="f32", buckets=None,
-                 device=None, stream=None):
+    def __init__(self, *, d, N, n=0, r=4, K=0, eta, seed, grad_dtype="f32", buckets=None,
+                 tensors=None, device=None, stream=None):
         import torch
         self.device = torch.device(device or "cuda")
         self.stream = stream or torch.cuda.current_stream(self.device)
         dt = ARC_DTYPE_BF16 if grad_dtype == "bf16" else ARC_DTYPE_F32
         cfg, keep = make_config(d=d, N=N, n=n, r=r, K=K, eta=eta, seed=seed, grad_dtype=dt,
-                                buckets=buckets)
+                                buckets=buckets, tensors=tensors)
         with torch.cuda.device(self.device):
             self.ctx = arc_create(cfg, self.stream)
         del keep
         self.d, self.N, self.n, self.r = d, N, n, r
+        self.tensors = None if tensors is None else [tuple(map(int, x)) for x in tensors]
         self.m = arc_num_rows(self.ctx)
         self.K_total = arc_selected_rows(self.ctx)
+        self.payload = arc_payload_elems(self.ctx)
         self.idx = torch.empty(max(self.K_total, 1), dtype=torch.int32, device=self.device)
-        self.agg = torch.empty((max(self.K_total, 1), n), dtype=torch.float32, device=self.device)
+        self.agg = torch.empty(max(self.payload, 1), dtype=torch.float32, device=self.device)
 
     def step(self, t, grad, h, g):
         arc_step(self.ctx, t, grad, h, g, self.idx, self.agg)
-        return self.idx[: self.K_total], self.agg[: self.K_total]
+        agg = self.agg[: self.payload]
+        if self.tensors is None:
+            agg = agg.view(self.K_total, self.n)
+        return self.idx[: self.K_total], agg
 
     def describe(self):
         return arc_describe(self.ctx)

@@ -36,6 +36,14 @@ ARC_NUM_STAGES = 5
 STAGE_NAMES = ("sketch", "reduce", "select", "gather_update", "step")
 
 
+class arc_tensor(ctypes.Structure):
+    _fields_ = [
+        ("rows", ctypes.c_int64),
+        ("cols", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+    ]
+
+
 class arc_config(ctypes.Structure):
     _fields_ = [
         ("d", ctypes.c_int64),
@@ -50,6 +58,9 @@ class arc_config(ctypes.Structure):
         ("num_buckets", ctypes.c_int32),
         ("eta", ctypes.c_float),
         ("reserved", ctypes.c_int32),
+        ("tensors", ctypes.POINTER(arc_tensor)),
+        ("num_tensors", ctypes.c_int32),
+        ("reserved2", ctypes.c_int32),
     ]
 
 
@@ -61,6 +72,9 @@ _SIGS = {
     "arc_destroy": (_st, [_vp]),
     "arc_num_rows": (ctypes.c_int64, [_vp]),
     "arc_selected_rows": (ctypes.c_int64, [_vp]),
+    "arc_payload_elems": (ctypes.c_int64, [_vp]),
+    "arc_projection": (_st, [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                             _vp]),
     "arc_status_str": (ctypes.c_char_p, [_st]),
     "arc_last_error": (ctypes.c_char_p, []),
     "arc_describe": (_st, [_vp, ctypes.c_char_p, ctypes.c_int64]),
@@ -105,15 +119,17 @@ def _addr(x):
     raise TypeError(f"cannot take the address of {type(x)!r}")
 
 
-def make_config(*, d: int, N: int, n: int, r: int = 4, K: int = 0, eta: float,
-                seed: int, grad_dtype: int = ARC_DTYPE_F32, buckets=None,
-                reserved: int = 0):
-    """Build an ``arc_config``; ``buckets`` = (row_begin[nb+1], K[nb]) or None.
-    Returns (config, keepalive) - keep the second value alive until arc_create
-    returns (it owns the bucket arrays)."""
+def make_config(*, d: int, N: int, n: int = 0, r: int = 4, K: int = 0, eta: float,
+                seed: int, grad_dtype: int = ARC_DTYPE_F32, buckets=None, tensors=None,
+                reserved: int = 0, reserved2: int = 0):
+    """Build an ``arc_config``; ``buckets`` = (row_begin[nb+1], K[nb]) or None;
+    ``tensors`` = [(rows, cols, K), ...] for the per-tensor mode (then n, K
+    and buckets stay 0 / None).  Returns (config, keepalive) - keep the second
+    value alive until arc_create returns (it owns the arrays)."""
     cfg = arc_config(d=d, n=n, K=K, seed=seed & (2**64 - 1), N=N, r=r,
-                     grad_dtype=grad_dtype, num_buckets=0, eta=eta, reserved=reserved)
-    keep = None
+                     grad_dtype=grad_dtype, num_buckets=0, eta=eta, reserved=reserved,
+                     num_tensors=0, reserved2=reserved2)
+    keep = []
     if buckets is not None:
         begin, ks = buckets
         b_arr = (ctypes.c_int64 * len(begin))(*begin)
@@ -121,7 +137,13 @@ def make_config(*, d: int, N: int, n: int, r: int = 4, K: int = 0, eta: float,
         cfg.bucket_row_begin = ctypes.cast(b_arr, ctypes.POINTER(ctypes.c_int64))
         cfg.bucket_K = ctypes.cast(k_arr, ctypes.POINTER(ctypes.c_int64))
         cfg.num_buckets = len(ks)
-        keep = (b_arr, k_arr)
+        keep += [b_arr, k_arr]
+    if tensors is not None:
+        t_arr = (arc_tensor * len(tensors))(*[arc_tensor(int(a), int(b), int(c))
+                                             for a, b, c in tensors])
+        cfg.tensors = ctypes.cast(t_arr, ctypes.POINTER(arc_tensor))
+        cfg.num_tensors = len(tensors)
+        keep.append(t_arr)
     return cfg, keep
 
 
@@ -149,6 +171,15 @@ def arc_num_rows(ctx) -> int:
 
 def arc_selected_rows(ctx) -> int:
     return int(_lib.arc_selected_rows(ctx))
+
+
+def arc_payload_elems(ctx) -> int:
+    return int(_lib.arc_payload_elems(ctx))
+
+
+def arc_projection(seed: int, t: int, n: int, r: int, out_V) -> None:
+    """V_t of width n for a shared seed into host memory (numpy [n, r] f32)."""
+    _check(_lib.arc_projection(seed & (2**64 - 1), t, n, r, _addr(out_V)), "arc_projection")
 
 
 def arc_status_str(status: int) -> str:

@@ -1,5 +1,11 @@
 // libarctopk C ABI: configuration checks, device workspace, and the per-step
 // enqueue of the ARC-Top-K + EF21M pipeline on the caller's HIP stream.
+//
+// Both layouts the library accepts -- one m x n view of the whole vector
+// (Eq. (3)) and one natural 2-D view per tensor -- are lowered at create time
+// to the same tables: row groups of up to 64 rows for the sketch kernels,
+// selection buckets for the arg-top-K, and (per-tensor mode) gather buckets
+// for the variable-width payload.
 #include <hip/hip_runtime.h>
 
 #include <array>
@@ -7,6 +13,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -28,13 +35,15 @@ arc_status fail_hip(hipError_t e, const char* where) {
   return e == hipErrorOutOfMemory ? ARC_ERR_NOMEM : ARC_ERR_DEVICE;
 }
 
-#define ARC_HIP(call, where)                          \
-  do {                                                \
-    const hipError_t arc_e_ = (call);                 \
+#define ARC_HIP(call, where)                                  \
+  do {                                                        \
+    const hipError_t arc_e_ = (call);                         \
     if (arc_e_ != hipSuccess) return fail_hip(arc_e_, where); \
   } while (0)
 
 constexpr int kEventsPerStep = 6;
+constexpr int64_t kGroupRows = 64;  // rows of one row group (one wave's rows)
+constexpr int32_t kMaxTensors = 1 << 24;
 
 bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
   const uintptr_t pa = reinterpret_cast<uintptr_t>(a);
@@ -46,29 +55,49 @@ bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
 }
 
+// r values the vectorised sketch kernels are instantiated for.
+bool vector_r(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8; }
+
+// Row widths the vectorised sketch kernels take: whole 32-column chunks, and
+// a 64-row group small enough for 32-bit byte offsets.
+bool vector_width(int64_t cols) { return cols % 32 == 0 && cols <= (int64_t{1} << 22); }
+
 }  // namespace
 
 struct arc_ctx {
   // problem
-  int64_t d = 0, n = 0, m = 0, m_full = 0;
+  int64_t d = 0, n = 0, m = 0;
   int32_t N = 0, r = 0, grad_bf16 = 0;
   float eta = 0.f, a = 0.f;
   uint64_t seed = 0;
-  int64_t K_total = 0;
+  bool tensor_mode = false;
+  int64_t K_total = 0, payload = 0;
   std::vector<arc::BucketDesc> buckets;
   std::vector<arc::BlockDesc> blocks;
+  // projection: one V_t per distinct row width, concatenated in first-use order
+  std::vector<int64_t> widths;
+  std::map<int64_t, int64_t> v_off;
+  int64_t v_floats = 0;
+  // row groups, the vectorisable ones first
+  std::vector<arc::RowGroup> groups;
+  int64_t nvec_groups = 0;
+  // per-tensor gather
+  std::vector<arc::GatherBucket> gather;
+  int64_t gather_work = 0;
   // device
   hipStream_t stream = nullptr;
   int device = 0;
+  size_t max_lds_per_block = 0;
   float* V_dev = nullptr;
   float* S_dev = nullptr;
   float* sigma_dev = nullptr;
+  arc::RowGroup* groups_dev = nullptr;
+  arc::GatherBucket* gather_dev = nullptr;
   arc::BucketDesc* buckets_dev = nullptr;
   arc::BlockDesc* blocks_dev = nullptr;
   arc::BucketState* state_dev = nullptr;
   uint32_t* hist_dev = nullptr;
   uint32_t* blockcnt_dev = nullptr;
-  size_t max_lds_per_block = 0;
   // projection staging: two pinned buffers, reused every other step
   float* V_pinned[2] = {nullptr, nullptr};
   hipEvent_t V_done[2] = {nullptr, nullptr};
@@ -80,6 +109,11 @@ struct arc_ctx {
   bool timing = false;
   std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
   size_t ev_used = 0;
+
+  bool fused_fits() const {
+    return N <= arc::kMaxFusedWorkers &&
+           arc::fused_sketch_lds_bytes(N) <= max_lds_per_block;
+  }
 
   arc::SelectWorkspace select_ws() const {
     arc::SelectWorkspace ws;
@@ -102,7 +136,8 @@ struct arc_ctx {
   void release() {
     (void)hipStreamSynchronize(stream);
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
-                    static_cast<void*>(sigma_dev), static_cast<void*>(buckets_dev),
+                    static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
+                    static_cast<void*>(gather_dev), static_cast<void*>(buckets_dev),
                     static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
                     static_cast<void*>(hist_dev), static_cast<void*>(blockcnt_dev)})
       if (p) (void)hipFree(p);
@@ -119,18 +154,45 @@ struct arc_ctx {
 
 namespace {
 
+// Per-tensor checks; m_out receives the total number of rows.
+arc_status check_tensors(const arc_config* cfg, int64_t* m_out) {
+  if (cfg->num_tensors > kMaxTensors) return fail(ARC_ERR_INVALID, "num_tensors exceeds 2^24");
+  if (cfg->tensors == nullptr) return fail(ARC_ERR_INVALID, "tensors is NULL");
+  if (cfg->n != 0 || cfg->K != 0 || cfg->num_buckets != 0)
+    return fail(ARC_ERR_INVALID, "per-tensor mode needs n == 0, K == 0 and num_buckets == 0");
+  int64_t covered = 0, m = 0;
+  for (int32_t b = 0; b < cfg->num_tensors; ++b) {
+    const arc_tensor& t = cfg->tensors[b];
+    if (t.rows < 1 || t.cols < 1 || t.K < 0)
+      return fail(ARC_ERR_INVALID, "tensor rows and cols must be >= 1 and K >= 0");
+    if (t.cols > INT32_MAX) return fail(ARC_ERR_INVALID, "tensor cols must be < 2^31");
+    if (t.rows > (cfg->d - covered) / t.cols)
+      return fail(ARC_ERR_INVALID, "tensors cover more than d coordinates");
+    covered += t.rows * t.cols;
+    m += t.rows;
+  }
+  if (covered != cfg->d) return fail(ARC_ERR_INVALID, "tensors must cover exactly d coordinates");
+  if (m > INT32_MAX) return fail(ARC_ERR_INVALID, "total rows exceed 2^31-1");
+  *m_out = m;
+  return ARC_OK;
+}
+
 // Configuration checks shared by arc_create; no HIP call is made here.
 arc_status check_config(const arc_config* cfg, int64_t* m_out) {
   if (cfg == nullptr) return fail(ARC_ERR_INVALID, "cfg is NULL");
   if (cfg->d <= 0) return fail(ARC_ERR_INVALID, "d must be > 0");
-  if (cfg->n <= 0) return fail(ARC_ERR_INVALID, "n must be > 0");
   if (cfg->N <= 0 || cfg->N > 65535) return fail(ARC_ERR_INVALID, "N must be in 1..65535");
   if (cfg->r <= 0 || cfg->r > ARC_MAX_R) return fail(ARC_ERR_INVALID, "r must be in 1..ARC_MAX_R");
   if (cfg->grad_dtype != ARC_DTYPE_F32 && cfg->grad_dtype != ARC_DTYPE_BF16)
     return fail(ARC_ERR_INVALID, "grad_dtype must be ARC_DTYPE_F32 or ARC_DTYPE_BF16");
   if (!(cfg->eta >= 0.0f && cfg->eta <= 1.0f)) return fail(ARC_ERR_INVALID, "eta must be in [0, 1]");
-  if (cfg->reserved != 0) return fail(ARC_ERR_INVALID, "reserved must be 0");
+  if (cfg->reserved != 0 || cfg->reserved2 != 0)
+    return fail(ARC_ERR_INVALID, "reserved fields must be 0");
   if (cfg->d > INT64_MAX / cfg->N) return fail(ARC_ERR_INVALID, "N*d overflows");
+  if (cfg->num_tensors < 0) return fail(ARC_ERR_INVALID, "num_tensors must be >= 0");
+  if (cfg->num_tensors > 0) return check_tensors(cfg, m_out);
+  if (cfg->n <= 0) return fail(ARC_ERR_INVALID, "n must be > 0");
+  if (cfg->n > INT32_MAX) return fail(ARC_ERR_INVALID, "n must be < 2^31");
   const int64_t m = cfg->d / cfg->n + (cfg->d % cfg->n != 0);
   if (m > INT32_MAX) return fail(ARC_ERR_INVALID, "m = ceil(d/n) exceeds 2^31-1");
   if (cfg->num_buckets < 0) return fail(ARC_ERR_INVALID, "num_buckets must be >= 0");
@@ -151,23 +213,21 @@ arc_status check_config(const arc_config* cfg, int64_t* m_out) {
   return ARC_OK;
 }
 
-void build_selection_plan(const arc_config* cfg, arc_ctx* c) {
-  const int32_t nb = cfg->num_buckets == 0 ? 1 : cfg->num_buckets;
+// Selection buckets from row boundaries begin[0..nb] and requested K's.
+// Fat blocks (few blocks per bucket keep the per-bin atomics and the
+// block-prefix sums short), at most kMaxBlocksPerBucket of them per bucket.
+void build_selection_plan(const std::vector<int64_t>& begin, const std::vector<int64_t>& want,
+                          arc_ctx* c) {
   int64_t out = 0;
-  for (int32_t b = 0; b < nb; ++b) {
+  for (size_t b = 0; b < want.size(); ++b) {
     arc::BucketDesc bd{};
-    bd.lo = cfg->num_buckets == 0 ? 0 : cfg->bucket_row_begin[b];
-    bd.hi = cfg->num_buckets == 0 ? c->m : cfg->bucket_row_begin[b + 1];
-    const int64_t want = cfg->num_buckets == 0 ? cfg->K : cfg->bucket_K[b];
-    bd.k = want < bd.hi - bd.lo ? want : bd.hi - bd.lo;
-    bd.out_off = out;
-    bd.mode = bd.k == 0 ? arc::kSelectNone
-              : bd.k == bd.hi - bd.lo ? arc::kSelectAll : arc::kSelectRadix;
-    // Fat blocks (few blocks per bucket keep the per-bin atomics and the
-    // block-prefix sums short), at most kMaxBlocksPerBucket of them.
+    bd.lo = begin[b];
+    bd.hi = begin[b + 1];
     const int64_t rows = bd.hi - bd.lo;
-    const int64_t per_block_cap =
-        (int64_t)arc::kSelectThreads * arc::kMaxBlocksPerBucket;
+    bd.k = want[b] < rows ? want[b] : rows;
+    bd.out_off = out;
+    bd.mode = bd.k == 0 ? arc::kSelectNone : bd.k == rows ? arc::kSelectAll : arc::kSelectRadix;
+    const int64_t per_block_cap = (int64_t)arc::kSelectThreads * arc::kMaxBlocksPerBucket;
     int64_t rpt = (rows + per_block_cap - 1) / per_block_cap;
     if (rpt < arc::kMinRowsPerThread) rpt = arc::kMinRowsPerThread;
     const int64_t rows_per_block = rpt * arc::kSelectThreads;
@@ -177,7 +237,7 @@ void build_selection_plan(const arc_config* cfg, arc_ctx* c) {
       arc::BlockDesc blk{};
       blk.lo = lo;
       blk.hi = lo + rows_per_block < bd.hi ? lo + rows_per_block : bd.hi;
-      blk.bucket = b;
+      blk.bucket = static_cast<int32_t>(b);
       c->blocks.push_back(blk);
     }
     bd.nblk = static_cast<int32_t>(c->blocks.size()) - bd.first_blk;
@@ -185,6 +245,104 @@ void build_selection_plan(const arc_config* cfg, arc_ctx* c) {
     c->buckets.push_back(bd);
   }
   c->K_total = out;
+}
+
+struct GroupLists {
+  std::vector<arc::RowGroup> vec, general;
+};
+
+// Row groups over `rows` rows of width `cols` that start at coordinate
+// elem_off and global row row0; the last row holds last_len <= cols values.
+// Groups are vectorisable when `vec` holds and they have no ragged row.
+void add_groups(int64_t elem_off, int64_t row0, int64_t rows, int64_t cols, int64_t last_len,
+                int64_t v_off, bool vec, GroupLists* out) {
+  for (int64_t p = 0; p < rows; p += kGroupRows) {
+    arc::RowGroup grp{};
+    grp.elem_off = elem_off + p * cols;
+    grp.row0 = row0 + p;
+    grp.v_off = v_off;
+    grp.rows = static_cast<int32_t>(rows - p < kGroupRows ? rows - p : kGroupRows);
+    grp.cols = static_cast<int32_t>(cols);
+    grp.last_len = static_cast<int32_t>(p + grp.rows == rows ? last_len : cols);
+    (vec && grp.last_len == grp.cols ? out->vec : out->general).push_back(grp);
+  }
+}
+
+// Lowers the configuration to the kernels' tables (host side only).
+void build_plan(const arc_config* cfg, arc_ctx* c) {
+  GroupLists lists;
+  std::vector<int64_t> begin{0}, want;
+  if (!c->tensor_mode) {
+    // One m x n view (Eq. (3)); rows [0, m_full) are whole, row m_full (if
+    // any) holds the d - m_full*n remaining coordinates.
+    c->widths.push_back(c->n);
+    c->v_off[c->n] = 0;
+    c->v_floats = c->n * c->r;
+    const int64_t m_full = c->d / c->n;
+    if (vector_width(c->n) && c->d % 4 == 0 && vector_r(c->r)) {
+      add_groups(0, 0, m_full, c->n, c->n, 0, true, &lists);
+      if (c->m > m_full)
+        add_groups(m_full * c->n, m_full, 1, c->n, c->d - m_full * c->n, 0, false, &lists);
+    } else {
+      add_groups(0, 0, c->m, c->n, c->d - (c->m - 1) * c->n, 0, false, &lists);
+    }
+    if (cfg->num_buckets == 0) {
+      begin.push_back(c->m);
+      want.push_back(cfg->K);
+    } else {
+      for (int32_t b = 0; b < cfg->num_buckets; ++b) {
+        begin.push_back(cfg->bucket_row_begin[b + 1]);
+        want.push_back(cfg->bucket_K[b]);
+      }
+    }
+    build_selection_plan(begin, want, c);
+    c->payload = c->K_total * c->n;
+  } else {
+    // One view per tensor; tensors of equal width share one V_t.
+    for (int32_t b = 0; b < cfg->num_tensors; ++b) {
+      const int64_t w = cfg->tensors[b].cols;
+      if (c->v_off.emplace(w, c->v_floats).second) {
+        c->widths.push_back(w);
+        c->v_floats += w * c->r;
+      }
+    }
+    int64_t off = 0, row0 = 0;
+    for (int32_t b = 0; b < cfg->num_tensors; ++b) {
+      const arc_tensor& t = cfg->tensors[b];
+      const bool vec = vector_width(t.cols) && off % 4 == 0 && c->d % 4 == 0 && vector_r(c->r);
+      add_groups(off, row0, t.rows, t.cols, t.cols, c->v_off[t.cols], vec, &lists);
+      off += t.rows * t.cols;
+      row0 += t.rows;
+      begin.push_back(row0);
+      want.push_back(t.K);
+    }
+    build_selection_plan(begin, want, c);
+    int64_t agg_off = 0, work = 0;
+    off = 0;
+    for (int32_t b = 0; b < cfg->num_tensors; ++b) {
+      const arc_tensor& t = cfg->tensors[b];
+      const arc::BucketDesc& bd = c->buckets[b];
+      arc::GatherBucket gb{};
+      gb.row0 = bd.lo;
+      gb.elem_off = off;
+      gb.out_off = bd.out_off;
+      gb.agg_off = agg_off;
+      gb.work_off = work;
+      gb.rows = t.rows;
+      gb.cols = static_cast<int32_t>(t.cols);
+      gb.k = static_cast<int32_t>(bd.k);
+      gb.vec = t.cols % 4 == 0 && off % 4 == 0 && agg_off % 4 == 0 && c->d % 4 == 0;
+      c->gather.push_back(gb);
+      agg_off += bd.k * t.cols;
+      work += bd.k * ((t.cols + 3) / 4);
+      off += t.rows * t.cols;
+    }
+    c->payload = agg_off;
+    c->gather_work = work;
+  }
+  c->nvec_groups = static_cast<int64_t>(lists.vec.size());
+  c->groups = std::move(lists.vec);
+  c->groups.insert(c->groups.end(), lists.general.begin(), lists.general.end());
 }
 
 template <typename T>
@@ -199,13 +357,19 @@ arc_status dev_alloc(T** p, size_t count, const char* what) {
   return ARC_OK;
 }
 
+template <typename T>
+hipError_t upload(T* dst, const std::vector<T>& src) {
+  if (src.empty()) return hipSuccess;
+  return hipMemcpy(dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+}
+
 arc_status record(arc_ctx* c, size_t slot, int which) {
   if (!c->timing) return ARC_OK;
   ARC_HIP(hipEventRecord(c->ev_pool[slot][which], c->stream), "hipEventRecord");
   return ARC_OK;
 }
 
-// Pinned staging + async copy of this step's projection.
+// Pinned staging + async copy of this step's projections.
 arc_status upload_projection(arc_ctx* c, int64_t t) {
   const int s = c->V_slot;
   c->V_slot ^= 1;
@@ -213,12 +377,13 @@ arc_status upload_projection(arc_ctx* c, int64_t t) {
     ARC_HIP(hipEventSynchronize(c->V_done[s]), "hipEventSynchronize(projection)");
     c->V_pending[s] = false;
   }
-  const size_t count = static_cast<size_t>(c->n) * c->r;
-  if (c->use_override)
-    std::memcpy(c->V_pinned[s], c->V_override.data(), count * sizeof(float));
-  else
-    arc::generate_projection(c->seed, t, c->n, c->r, c->V_pinned[s]);
-  ARC_HIP(hipMemcpyAsync(c->V_dev, c->V_pinned[s], count * sizeof(float),
+  if (c->use_override) {
+    std::memcpy(c->V_pinned[s], c->V_override.data(), c->V_override.size() * sizeof(float));
+  } else {
+    for (int64_t w : c->widths)
+      arc::generate_projection(c->seed, t, w, c->r, c->V_pinned[s] + c->v_off[w]);
+  }
+  ARC_HIP(hipMemcpyAsync(c->V_dev, c->V_pinned[s], static_cast<size_t>(c->v_floats) * sizeof(float),
                          hipMemcpyHostToDevice, c->stream),
           "hipMemcpyAsync(projection)");
   ARC_HIP(hipEventRecord(c->V_done[s], c->stream), "hipEventRecord(projection)");
@@ -243,6 +408,15 @@ const char* arc_status_str(arc_status s) {
 
 const char* arc_last_error(void) { return g_last_error.c_str(); }
 
+arc_status arc_projection(uint64_t seed, int64_t t, int64_t n, int32_t r, float* V) {
+  if (V == nullptr) return fail(ARC_ERR_INVALID, "V is NULL");
+  if (t < 0) return fail(ARC_ERR_INVALID, "t must be >= 0");
+  if (n < 1) return fail(ARC_ERR_INVALID, "n must be >= 1");
+  if (r < 1 || r > ARC_MAX_R) return fail(ARC_ERR_INVALID, "r must be in 1..ARC_MAX_R");
+  arc::generate_projection(seed, t, n, r, V);
+  return ARC_OK;
+}
+
 arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   if (out == nullptr) return fail(ARC_ERR_INVALID, "out is NULL");
   *out = nullptr;
@@ -254,9 +428,9 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   if (c == nullptr) return fail(ARC_ERR_NOMEM, "host allocation failed");
   try {
     c->d = cfg->d;
-    c->n = cfg->n;
+    c->tensor_mode = cfg->num_tensors > 0;
+    c->n = c->tensor_mode ? 0 : cfg->n;
     c->m = m;
-    c->m_full = cfg->d / cfg->n;
     c->N = cfg->N;
     c->r = cfg->r;
     c->grad_bf16 = cfg->grad_dtype == ARC_DTYPE_BF16;
@@ -264,7 +438,7 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
     c->a = 1.0f - cfg->eta;
     c->seed = cfg->seed;
     c->stream = static_cast<hipStream_t>(hip_stream);
-    build_selection_plan(cfg, c);
+    build_plan(cfg, c);
   } catch (...) {
     delete c;
     return fail(ARC_ERR_NOMEM, "host allocation failed");
@@ -277,11 +451,17 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   };
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) return bail(fail_hip(e, "hipGetDevice"));
+  int lds_limit = 0;
+  e = hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device);
+  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
+  c->max_lds_per_block = static_cast<size_t>(lds_limit);
 
   const size_t nb = c->buckets.size(), nblk = c->blocks.size();
-  if ((st = dev_alloc(&c->V_dev, static_cast<size_t>(c->n) * c->r, "hipMalloc(V)")) ||
+  if ((st = dev_alloc(&c->V_dev, static_cast<size_t>(c->v_floats), "hipMalloc(V)")) ||
       (st = dev_alloc(&c->S_dev, static_cast<size_t>(c->N) * c->m * c->r, "hipMalloc(S)")) ||
       (st = dev_alloc(&c->sigma_dev, static_cast<size_t>(c->m), "hipMalloc(sigma)")) ||
+      (st = dev_alloc(&c->groups_dev, c->groups.size(), "hipMalloc(groups)")) ||
+      (st = dev_alloc(&c->gather_dev, c->gather.size(), "hipMalloc(gather)")) ||
       (st = dev_alloc(&c->buckets_dev, nb, "hipMalloc(buckets)")) ||
       (st = dev_alloc(&c->blocks_dev, nblk, "hipMalloc(blocks)")) ||
       (st = dev_alloc(&c->state_dev, nb, "hipMalloc(state)")) ||
@@ -289,14 +469,9 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
                       "hipMalloc(hist)")) ||
       (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")))
     return bail(st);
-  int lds_limit = 0;
-  e = hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock,
-                            c->device);
-  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
-  c->max_lds_per_block = static_cast<size_t>(lds_limit);
   for (int s = 0; s < 2; ++s) {
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
-                      static_cast<size_t>(c->n) * c->r * sizeof(float), hipHostMallocDefault);
+                      static_cast<size_t>(c->v_floats) * sizeof(float), hipHostMallocDefault);
     if (e != hipSuccess) {
       c->V_pinned[s] = nullptr;
       return bail(fail_hip(e, "hipHostMalloc(projection)"));
@@ -307,16 +482,14 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
       return bail(fail_hip(e, "hipEventCreate"));
     }
   }
-  // Constant selection tables, and zeroed radix scratch (kept zero between
-  // uses by the kernels themselves).
-  e = hipMemcpy(c->buckets_dev, c->buckets.data(), nb * sizeof(arc::BucketDesc),
-                hipMemcpyHostToDevice);
+  // Constant tables, and zeroed radix scratch (kept zero between uses by the
+  // kernels themselves).
+  e = upload(c->buckets_dev, c->buckets);
+  if (e == hipSuccess) e = upload(c->blocks_dev, c->blocks);
+  if (e == hipSuccess) e = upload(c->groups_dev, c->groups);
+  if (e == hipSuccess) e = upload(c->gather_dev, c->gather);
   if (e == hipSuccess)
-    e = hipMemcpy(c->blocks_dev, c->blocks.data(), nblk * sizeof(arc::BlockDesc),
-                  hipMemcpyHostToDevice);
-  if (e == hipSuccess)
-    e = hipMemset(c->hist_dev, 0,
-                  arc::kRadixPasses * nb * arc::kRadixBins * sizeof(uint32_t));
+    e = hipMemset(c->hist_dev, 0, arc::kRadixPasses * nb * arc::kRadixBins * sizeof(uint32_t));
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) return bail(fail_hip(e, "workspace initialisation"));
   *out = c;
@@ -334,6 +507,8 @@ int64_t arc_num_rows(const arc_ctx* ctx) { return ctx ? ctx->m : -1; }
 
 int64_t arc_selected_rows(const arc_ctx* ctx) { return ctx ? ctx->K_total : -1; }
 
+int64_t arc_payload_elems(const arc_ctx* ctx) { return ctx ? ctx->payload : -1; }
+
 arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
                     int32_t* out_idx, float* out_agg) {
   if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
@@ -349,11 +524,11 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
       ranges_overlap(h, state_bytes, g, state_bytes))
     return fail(ARC_ERR_INVALID, "grad, h and g must not overlap");
 
-  const bool vec_ok = c->n % 32 == 0 && c->d % 4 == 0 && aligned16(grad) &&
-                      aligned16(h) && aligned16(g);
-  const bool fast_sketch = vec_ok && (c->r == 1 || c->r == 2 || c->r == 4 || c->r == 8);
-  const bool fast_gather = c->n % 4 == 0 && c->d % 4 == 0 && aligned16(h) &&
-                           aligned16(g) && aligned16(out_agg);
+  // Vectorisable groups take the 16-byte kernels only when the three streams
+  // are 16-byte aligned; otherwise every group takes the general kernel.
+  const int64_t ngroups = static_cast<int64_t>(c->groups.size());
+  const int64_t nvec = aligned16(grad) && aligned16(h) && aligned16(g) ? c->nvec_groups : 0;
+  const bool fused = nvec > 0 && c->fused_fits();
 
   size_t slot = 0;
   if (c->timing) {
@@ -369,59 +544,68 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
   if ((st = upload_projection(c, t))) return st;
   if ((st = record(c, slot, 1))) return st;
   // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
-  // the same kernel also forms the worker sum and importance of its rows.
-  const int64_t fast_rows = fast_sketch ? c->m_full : 0;
-  const bool fused = fast_sketch && c->N <= arc::kMaxFusedWorkers &&
-                     arc::fused_sketch_lds_bytes(c->N) <= c->max_lds_per_block;
+  // the fused kernel also forms the worker sum and importance of its rows.
   if (fused) {
-    ARC_HIP(arc::launch_sketch_fused(grad, c->grad_bf16, h, g, c->V_dev, c->S_dev,
-                                     c->sigma_dev, c->d, c->n, c->m, c->N, c->r, 0,
-                                     fast_rows, c->eta, c->a, c->stream),
+    ARC_HIP(arc::launch_sketch_fused(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev, nvec,
+                                     c->S_dev, c->sigma_dev, c->d, c->m, c->N, c->r, c->eta,
+                                     c->a, c->stream),
             "fused sketch launch");
   } else {
-    ARC_HIP(arc::launch_sketch(fast_sketch, grad, c->grad_bf16, h, g, c->V_dev,
-                               c->S_dev, c->d, c->n, c->m, c->N, c->r, 0, fast_rows,
-                               c->eta, c->a, c->stream),
+    ARC_HIP(arc::launch_sketch(true, grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev, nvec,
+                               c->S_dev, c->d, c->m, c->N, c->r, c->eta, c->a, c->stream),
             "sketch launch");
   }
-  ARC_HIP(arc::launch_sketch(false, grad, c->grad_bf16, h, g, c->V_dev, c->S_dev, c->d,
-                             c->n, c->m, c->N, c->r, fast_rows, c->m, c->eta, c->a,
-                             c->stream),
+  ARC_HIP(arc::launch_sketch(false, grad, c->grad_bf16, h, g, c->V_dev,
+                             c->groups_dev + nvec, ngroups - nvec, c->S_dev, c->d, c->m, c->N,
+                             c->r, c->eta, c->a, c->stream),
           "sketch launch (general rows)");
   if ((st = record(c, slot, 2))) return st;
-  // Stage 1: worker sum + importance for the rows the fused kernel did not do.
-  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->m, c->N, c->r,
-                                        fused ? fast_rows : 0, c->m, c->stream),
+  // Stage 1: worker sum + importance of the rows the fused kernel did not do.
+  const int64_t done = fused ? nvec : 0;
+  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + done,
+                                        ngroups - done, c->m, c->N, c->r, c->stream),
           "reduce launch");
   if ((st = record(c, slot, 3))) return st;
-  const arc::SelectWorkspace ws = c->select_ws();
   // Stage 2: per-bucket top-K.
+  const arc::SelectWorkspace ws = c->select_ws();
   ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
   if ((st = record(c, slot, 4))) return st;
   // Stage 3: gather + worker sum + error-feedback update.
-  ARC_HIP(arc::launch_gather_update(fast_gather, h, g, out_idx, out_agg, c->K_total,
-                                    c->d, c->n, c->m, c->N, c->stream),
-          "gather launch");
+  if (c->tensor_mode) {
+    const bool vec_ok = aligned16(h) && aligned16(g) && aligned16(out_agg);
+    ARC_HIP(arc::launch_gather_update_tensors(h, g, out_idx, out_agg, c->gather_dev,
+                                              static_cast<int32_t>(c->gather.size()),
+                                              c->gather_work, c->d, c->N, vec_ok, c->stream),
+            "gather launch");
+  } else {
+    const bool fast_gather = c->n % 4 == 0 && c->d % 4 == 0 && aligned16(h) && aligned16(g) &&
+                             aligned16(out_agg);
+    ARC_HIP(arc::launch_gather_update(fast_gather, h, g, out_idx, out_agg, c->K_total, c->d,
+                                      c->n, c->m, c->N, c->stream),
+            "gather launch");
+  }
   if ((st = record(c, slot, 5))) return st;
   return ARC_OK;
 }
 
 arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
   if (c == nullptr || buf == nullptr || len <= 0) return fail(ARC_ERR_INVALID, "NULL argument");
-  const bool vec_shape = c->n % 32 == 0 && c->d % 4 == 0 &&
-                         (c->r == 1 || c->r == 2 || c->r == 4 || c->r == 8);
-  const bool fused = vec_shape && c->N <= arc::kMaxFusedWorkers &&
-                     arc::fused_sketch_lds_bytes(c->N) <= c->max_lds_per_block;
-  const char* sketch = !vec_shape ? "general" : (fused ? "fused" : "per_worker+reduce");
+  const int64_t ngroups = static_cast<int64_t>(c->groups.size());
+  const char* sketch = c->nvec_groups == 0 ? "general"
+                       : c->fused_fits()   ? "fused"
+                                           : "per_worker+reduce";
   int radix = 0;
   for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
   std::snprintf(buf, static_cast<size_t>(len),
-                "sketch=%s rows_vectorised=%lld rows_general=%lld fused_lds_bytes=%zu "
-                "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld",
-                sketch, static_cast<long long>(vec_shape ? c->m_full : 0),
-                static_cast<long long>(vec_shape ? c->m - c->m_full : c->m),
+                "mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
+                "general_groups=%lld fused_lds_bytes=%zu lds_limit=%zu buckets=%zu "
+                "radix_buckets=%d select_blocks=%zu K_total=%lld payload=%lld",
+                c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
+                static_cast<long long>(ngroups), static_cast<long long>(c->nvec_groups),
+                static_cast<long long>(ngroups - c->nvec_groups),
                 arc::fused_sketch_lds_bytes(c->N), c->max_lds_per_block, c->buckets.size(),
-                radix, c->blocks.size(), static_cast<long long>(c->K_total));
+                radix, c->blocks.size(), static_cast<long long>(c->K_total),
+                static_cast<long long>(c->payload));
   return ARC_OK;
 }
 
@@ -445,6 +629,8 @@ arc_status arc_debug_sketch(arc_ctx* c, float* out_S) {
 arc_status arc_debug_projection(arc_ctx* c, int64_t t, float* out_V) {
   if (c == nullptr || out_V == nullptr) return fail(ARC_ERR_INVALID, "NULL argument");
   if (t < 0) return fail(ARC_ERR_INVALID, "t must be >= 0");
+  if (c->tensor_mode)
+    return fail(ARC_ERR_UNSUPPORTED, "per-tensor mode: use arc_projection with the width");
   if (c->use_override)
     std::memcpy(out_V, c->V_override.data(), c->V_override.size() * sizeof(float));
   else
@@ -454,6 +640,7 @@ arc_status arc_debug_projection(arc_ctx* c, int64_t t, float* out_V) {
 
 arc_status arc_set_projection(arc_ctx* c, const float* V) {
   if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
+  if (c->tensor_mode) return fail(ARC_ERR_UNSUPPORTED, "arc_set_projection: per-tensor mode");
   if (V == nullptr) {
     c->use_override = false;
     c->V_override.clear();

@@ -24,6 +24,42 @@ __device__ __forceinline__ void stream_store(float4* p, float4 v) {
   __builtin_nontemporal_store(w, reinterpret_cast<f32x4_t*>(p));
 }
 
+// Raw buffer resource (stride 0) over `bytes` bytes from `base`.  Vector
+// memory instructions through it are range checked by the hardware on their
+// VGPR offset: a load at an offset >= bytes returns zero and a store there is
+// dropped.  Offsets are 32-bit byte offsets.
+typedef __amdgpu_buffer_rsrc_t buffer_rsrc;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+constexpr int kBufferDword3 = 0x00020000;  // gfx9-family raw buffer: 32-bit data format
+constexpr int kCacheDefault = 0;
+constexpr int kCacheNonTemporal = 2;       // nt cache-policy bit on gfx950
+
+__device__ __forceinline__ buffer_rsrc make_buffer(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           kBufferDword3);
+}
+
+template <int kPolicy>
+__device__ __forceinline__ float4 buffer_load_f4(buffer_rsrc r, uint32_t off) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kPolicy);
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+
+template <int kPolicy>
+__device__ __forceinline__ uint2 buffer_load_u2(buffer_rsrc r, uint32_t off) {
+  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kPolicy);
+  return make_uint2(v.x, v.y);
+}
+
+template <int kPolicy>
+__device__ __forceinline__ void buffer_store_f4(buffer_rsrc r, uint32_t off, float4 v) {
+  const u32x4_t w = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                     __float_as_uint(v.w)};
+  __builtin_amdgcn_raw_buffer_store_b128(w, r, (int)off, 0, kPolicy);
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs of the MI355X (block
 // b starts on XCD b % 8).  This bijection of [0, nblocks) hands each XCD one
 // contiguous range of blocks (the last nblocks % 8 map to themselves).

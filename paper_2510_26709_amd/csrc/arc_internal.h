@@ -49,6 +49,33 @@ struct BucketState {
   int64_t kleft;
 };
 
+// A group of up to 64 consecutive rows of one view (one wave's rows in the
+// sketch kernels).  Rows are `cols` wide and start `elem_off` coordinates into
+// each worker's vector; their projection is V[v_off .. v_off + cols*r).
+struct RowGroup {
+  int64_t elem_off;  // coordinate of the group's first element
+  int64_t row0;      // global index of the group's first row
+  int64_t v_off;     // offset of this width's projection in the V buffer
+  int32_t rows;      // 1..64
+  int32_t cols;      // row width
+  int32_t last_len;  // valid columns of the last row (< cols for a ragged tail)
+  int32_t pad;
+};
+
+// One tensor (selection bucket) of the per-tensor mode, for the gather.
+struct GatherBucket {
+  int64_t row0;      // global row of the tensor's first row
+  int64_t elem_off;  // coordinate of the tensor's first element
+  int64_t out_off;   // first position in out_idx
+  int64_t agg_off;   // first element in out_agg
+  int64_t work_off;  // first work item (one item = one row x 4 columns)
+  int64_t rows;      // rows of the tensor
+  int32_t cols;
+  int32_t k;         // rows kept
+  int32_t vec;       // 16-byte aligned rows and payload: float4 path
+  int32_t pad;
+};
+
 struct SelectWorkspace {
   const BucketDesc* buckets;
   const BlockDesc* blocks;
@@ -65,30 +92,32 @@ struct SelectWorkspace {
 // Bytes of LDS one block of the fused sketch kernel uses for N workers.
 size_t fused_sketch_lds_bytes(int32_t N);
 
-// Momentum + residual + per-worker sketch + worker sum + importance over full
-// rows [row_lo, row_hi), one block per 64 rows holding all N <= 8 workers.
-// Requires n % 32 == 0, d % 4 == 0, 16-byte aligned pointers, r in {1,2,4,8}.
+// Momentum + residual + per-worker sketch + worker sum + importance for the
+// row groups groups[0 .. ngroups): one block per group holding all N <= 8
+// workers.  Every group must be vectorisable (cols % 32 == 0, 16-byte aligned
+// rows, r in {1,2,4,8}, no ragged tail, rows*cols*4 < 2^31).
 hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
-                               const float* g, const float* V, float* S,
-                               float* sigma, int64_t d, int64_t n, int64_t m,
-                               int32_t N, int32_t r, int64_t row_lo,
-                               int64_t row_hi, float eta, float a,
+                               const float* g, const float* V,
+                               const RowGroup* groups, int64_t ngroups,
+                               float* S, float* sigma, int64_t d, int64_t m,
+                               int32_t N, int32_t r, float eta, float a,
                                hipStream_t stream);
 
-// Momentum + residual + per-worker sketch into S over rows [row_lo, row_hi).
-// fast != 0 selects the vectorised per-worker kernel (same requirements as
-// the fused one, any N); otherwise one thread per (row, worker).
+// Momentum + residual + per-worker sketch into S for groups[0 .. ngroups).
+// fast: the vectorised per-worker kernel (same requirements as the fused
+// one, any N); otherwise one thread per (row, worker), any group.
 hipError_t launch_sketch(bool fast, const void* grad, int32_t grad_bf16,
-                         float* h, const float* g, const float* V, float* S,
-                         int64_t d, int64_t n, int64_t m, int32_t N, int32_t r,
-                         int64_t row_lo, int64_t row_hi, float eta, float a,
-                         hipStream_t stream);
+                         float* h, const float* g, const float* V,
+                         const RowGroup* groups, int64_t ngroups, float* S,
+                         int64_t d, int64_t m, int32_t N, int32_t r, float eta,
+                         float a, hipStream_t stream);
 
-// P = sum_i S[i] (ascending i), sigma = row norm squared of P, rows
-// [row_lo, row_hi).
-hipError_t launch_reduce_importance(const float* S, float* sigma, int64_t m,
-                                    int32_t N, int32_t r, int64_t row_lo,
-                                    int64_t row_hi, hipStream_t stream);
+// P = sum_i S[i] (ascending i), sigma = row norm squared of P, for the rows
+// of groups[0 .. ngroups).
+hipError_t launch_reduce_importance(const float* S, float* sigma,
+                                    const RowGroup* groups, int64_t ngroups,
+                                    int64_t m, int32_t N, int32_t r,
+                                    hipStream_t stream);
 
 // Per-bucket arg-top-K of sigma into out_idx (ascending per bucket).
 hipError_t launch_select(const float* sigma, const SelectWorkspace& ws,
@@ -99,6 +128,13 @@ hipError_t launch_gather_update(bool fast, const float* h, float* g,
                                 const int32_t* idx, float* agg, int64_t K_total,
                                 int64_t d, int64_t n, int64_t m, int32_t N,
                                 hipStream_t stream);
+
+// Per-tensor mode gather: buckets[0 .. nb), work items total_work.
+hipError_t launch_gather_update_tensors(const float* h, float* g,
+                                        const int32_t* idx, float* agg,
+                                        const GatherBucket* buckets, int32_t nb,
+                                        int64_t total_work, int64_t d, int32_t N,
+                                        bool allow_vec, hipStream_t stream);
 
 // ---- host projection (arc_projection.cpp) ----
 // V_t (n x r, row-major) for the shared seed and step t.

@@ -24,51 +24,61 @@ constexpr int kRowF4 = 9;
 constexpr int kTileF4 = kWave * kRowF4;
 __device__ __forceinline__ int tile_slot(int rho, int q) { return rho * kRowF4 + q; }
 
-// One wave's pass over its 64 rows of worker i: loads the grad/h/g tile of
-// each 32-column chunk with coalesced 16-byte accesses, applies (11a), writes
-// h back, parks Delta in LDS, then runs this lane's r chains over its row.
-// FULL: all 64 rows exist (no per-row predicates).
-template <int R, bool BF16, bool FULL>
-__device__ __forceinline__ void sketch_rows_impl(
+// One wave's pass over the rows of one row group of worker i: loads the
+// grad/h/g tile of each 32-column chunk with coalesced 16-byte accesses,
+// applies (11a), writes h back, parks Delta in LDS, then runs this lane's r
+// chains over its row.  Local row l of the group starts at coordinate
+// elem_off + l*n.  The three streams are read through buffer resources that
+// end at the group's last row, so in a group of fewer than 64 rows the
+// missing rows read as zero (their lanes' sketches are discarded by the
+// caller) and are not stored.
+template <int R, bool BF16>
+__device__ __forceinline__ void sketch_rows(
     const void* __restrict__ grad, float* __restrict__ h,
     const float* __restrict__ g, const float* __restrict__ V, int64_t d,
-    int64_t n, int64_t p0, int64_t row_hi, int32_t i, float eta, float a,
-    float4* tile, float (&s)[R]) {
+    const RowGroup& grp, int32_t i, float eta, float a, float4* tile,
+    float (&s)[R]) {
   const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane >> 3;   // row within an 8-row slab
   const int quad = lane & 7;   // 16-byte column group within the chunk
-  const int64_t wbase = (int64_t)i * d;
+  const uint32_t n = (uint32_t)grp.cols;
+  const int32_t rows = grp.rows;
+  const int64_t wbase = (int64_t)i * d + grp.elem_off;
+  const uint32_t bytes = (uint32_t)rows * n * 4u;
+  const buffer_rsrc rh = make_buffer(h + wbase, bytes);
+  const buffer_rsrc rg = make_buffer(g + wbase, bytes);
+  const buffer_rsrc rx =
+      BF16 ? make_buffer(static_cast<const uint16_t*>(grad) + wbase, bytes / 2)
+           : make_buffer(static_cast<const float*>(grad) + wbase, bytes);
+  V += grp.v_off;
+  // byte offset of this lane's 16 bytes of binary32 in row u*8 + sub
+  uint32_t off[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * 8 + sub) * n + quad * 4) * 4u;
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
 
-  const int64_t nchunks = n / kChunk;
-  for (int64_t c = 0; c < nchunks; ++c) {
-    const int64_t col = c * kChunk + quad * 4;
+  const uint32_t nchunks = n / kChunk;
+  for (uint32_t c = 0; c < nchunks; ++c) {
     float4 xv[8], hv[8], gv[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int64_t p = p0 + u * 8 + sub;
-      const int64_t e = wbase + p * n + col;
-      if (FULL || p < row_hi) {
-        if constexpr (BF16) {
-          // 8-byte loads cover half a cache line whose other half belongs to
-          // the next chunk, so these stay cacheable.  (Counters show about
-          // half of those lines leave L2 twice; the second request is served
-          // by the last-level cache.  Loading both halves together removes it
-          // but costs occupancy and runs no faster.)
-          const uint2 w = *reinterpret_cast<const uint2*>(
-              static_cast<const uint16_t*>(grad) + e);
-          xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
-        } else {
-          xv[u] = stream_load(reinterpret_cast<const float4*>(
-              static_cast<const float*>(grad) + e));
-        }
-        hv[u] = *reinterpret_cast<const float4*>(h + e);
-        gv[u] = stream_load(reinterpret_cast<const float4*>(g + e));
+      if constexpr (BF16) {
+        // 8-byte loads cover half a cache line whose other half belongs to
+        // the next chunk, so these stay cacheable.  (Counters show about half
+        // of those lines leave L2 twice; the second request is served by the
+        // last-level cache.  Loading both halves together removes it but
+        // costs occupancy and runs no faster.)
+        const uint2 w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
+        xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
       } else {
-        xv[u] = hv[u] = gv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, off[u]);
       }
+      hv[u] = buffer_load_f4<kCacheDefault>(rh, off[u]);
+      gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, off[u]);
     }
+    // Keep all 24 loads of the chunk in flight before the first use.
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       float4 hn;
@@ -76,14 +86,14 @@ __device__ __forceinline__ void sketch_rows_impl(
       hn.y = fmaf(eta, xv[u].y, a * hv[u].y);
       hn.z = fmaf(eta, xv[u].z, a * hv[u].z);
       hn.w = fmaf(eta, xv[u].w, a * hv[u].w);
-      const int64_t p = p0 + u * 8 + sub;
-      if (FULL || p < row_hi) stream_store(reinterpret_cast<float4*>(h + wbase + p * n + col), hn);
+      if (u * 8 + sub < rows) buffer_store_f4<kCacheNonTemporal>(rh, off[u], hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
       dl.z = hn.z - gv[u].z;
       dl.w = hn.w - gv[u].w;
       tile[tile_slot(u * 8 + sub, quad)] = dl;
+      off[u] += kChunk * 4;
     }
     wave_lds_fence();
     const float* Vc = V + c * kChunk * R;
@@ -102,18 +112,6 @@ __device__ __forceinline__ void sketch_rows_impl(
   }
 }
 
-template <int R, bool BF16>
-__device__ __forceinline__ void sketch_rows(
-    const void* __restrict__ grad, float* __restrict__ h,
-    const float* __restrict__ g, const float* __restrict__ V, int64_t d,
-    int64_t n, int64_t p0, int64_t row_hi, int32_t i, float eta, float a,
-    float4* tile, float (&s)[R]) {
-  if (p0 + kWave <= row_hi)
-    sketch_rows_impl<R, BF16, true>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tile, s);
-  else
-    sketch_rows_impl<R, BF16, false>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tile, s);
-}
-
 // ---------------------------------------------------------------------------
 // Fused path: a block is N waves, wave i streams worker i over the same 64
 // rows; the waves then meet in LDS and wave 0 forms P = S^(0) + S^(1) + ...
@@ -126,18 +124,19 @@ template <int R, bool BF16>
 __global__ void __launch_bounds__(kMaxFusedWorkers * kWave)
 sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
                     const float* __restrict__ g, const float* __restrict__ V,
-                    float* __restrict__ S, float* __restrict__ sigma, int64_t d,
-                    int64_t n, int64_t m, int64_t row_lo, int64_t row_hi,
-                    int32_t N, float eta, float a) {
+                    const RowGroup* __restrict__ groups, float* __restrict__ S,
+                    float* __restrict__ sigma, int64_t d, int64_t m, int32_t N,
+                    float eta, float a) {
   extern __shared__ float4 lds_tiles[];  // N tiles of kTileF4
   const int lane = threadIdx.x & (kWave - 1);
   const int i = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // worker
-  const int64_t p0 = row_lo + xcd_contiguous_block(blockIdx.x, gridDim.x) * kWave;
+  const RowGroup grp = groups[xcd_contiguous_block(blockIdx.x, gridDim.x)];
   float4* tile = lds_tiles + i * kTileF4;
   float s[R];
-  sketch_rows<R, BF16>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tile, s);
-  const int64_t p = p0 + lane;
-  if (p < row_hi) {
+  sketch_rows<R, BF16>(grad, h, g, V, d, grp, i, eta, a, tile, s);
+  const bool mine = lane < grp.rows;
+  const int64_t p = grp.row0 + lane;
+  if (mine) {
     float* out = S + ((int64_t)i * m + p) * R;
 #pragma unroll
     for (int k = 0; k < R; ++k) out[k] = s[k];
@@ -147,7 +146,7 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
 #pragma unroll
   for (int k = 0; k < R; ++k) comb[k * kWave + lane] = s[k];
   __syncthreads();
-  if (i == 0 && p < row_hi) {
+  if (i == 0 && mine) {
     const float* base = reinterpret_cast<const float*>(lds_tiles);
     float acc = 0.0f;
 #pragma unroll
@@ -170,46 +169,47 @@ template <int R, bool BF16>
 __global__ void __launch_bounds__(kSketchWaves * kWave)
 sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
                          const float* __restrict__ g, const float* __restrict__ V,
-                         float* __restrict__ S, int64_t d, int64_t n, int64_t m,
-                         int64_t row_lo, int64_t row_hi, float eta, float a) {
+                         const RowGroup* __restrict__ groups, int64_t ngroups,
+                         float* __restrict__ S, int64_t d, int64_t m, float eta,
+                         float a) {
   __shared__ float4 tiles[kSketchWaves][kTileF4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t i = blockIdx.y;
-  const int64_t p0 =
-      row_lo + (xcd_contiguous_block(blockIdx.x, gridDim.x) * kSketchWaves + wave) * kWave;
-  if (p0 >= row_hi) return;  // whole wave; no block barrier follows
+  const int64_t gi = xcd_contiguous_block(blockIdx.x, gridDim.x) * kSketchWaves + wave;
+  if (gi >= ngroups) return;  // whole wave; no block barrier follows
+  const RowGroup grp = groups[gi];
   float s[R];
-  sketch_rows<R, BF16>(grad, h, g, V, d, n, p0, row_hi, i, eta, a, tiles[wave], s);
-  const int64_t p = p0 + lane;
-  if (p < row_hi) {
-    float* out = S + ((int64_t)i * m + p) * R;
+  sketch_rows<R, BF16>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
+  if (lane < grp.rows) {
+    float* out = S + ((int64_t)i * m + grp.row0 + lane) * R;
 #pragma unroll
     for (int k = 0; k < R; ++k) out[k] = s[k];
   }
 }
 
 // ---------------------------------------------------------------------------
-// General path: one thread per (row, worker); any n, d, r and alignment.  The
-// first pass updates h over the row; then, for each k, one pass re-reads h
-// (new) and g and runs that column's chain.
+// General path: one thread per (row, worker) of any row group; any width,
+// d, r and alignment, and ragged tails.  The first pass updates h over the
+// row; then, for each k, one pass re-reads h (new) and g and runs that
+// column's chain.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(kWave)
 sketch_generic_kernel(const void* __restrict__ grad, int32_t grad_bf16,
                       float* __restrict__ h, const float* __restrict__ g,
-                      const float* __restrict__ V, float* __restrict__ S,
-                      int64_t d, int64_t n, int64_t m, int32_t N, int32_t r,
-                      int64_t row_lo, int64_t row_hi, float eta, float a) {
-  const int64_t rows = row_hi - row_lo;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid >= rows * N) return;
-  const int32_t i = (int32_t)(tid / rows);
-  const int64_t p = row_lo + tid % rows;
-  const int64_t base = (int64_t)i * d;
-  const int64_t e0 = p * n;
-  const int64_t len = (e0 + n <= d) ? n : d - e0;
+                      const float* __restrict__ V,
+                      const RowGroup* __restrict__ groups, float* __restrict__ S,
+                      int64_t d, int64_t m, int32_t r, float eta, float a) {
+  const RowGroup grp = groups[blockIdx.x];
+  const int lane = threadIdx.x;
+  if (lane >= grp.rows) return;
+  const int32_t i = blockIdx.y;
+  const int64_t n = grp.cols;
+  const int64_t len = lane == grp.rows - 1 ? grp.last_len : n;
+  const int64_t base = (int64_t)i * d + grp.elem_off + lane * n;
+  const float* Vg = V + grp.v_off;
   for (int64_t j = 0; j < len; ++j) {
-    const int64_t e = base + e0 + j;
+    const int64_t e = base + j;
     float x;
     if (grad_bf16)
       x = __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e] << 16);
@@ -220,21 +220,23 @@ sketch_generic_kernel(const void* __restrict__ grad, int32_t grad_bf16,
   for (int32_t k = 0; k < r; ++k) {
     float s = 0.0f;
     for (int64_t j = 0; j < len; ++j) {
-      const int64_t e = base + e0 + j;
+      const int64_t e = base + j;
       const float dl = h[e] - g[e];
-      s = fmaf(dl, V[j * r + k], s);
+      s = fmaf(dl, Vg[j * r + k], s);
     }
-    S[((int64_t)i * m + p) * r + k] = s;
+    S[((int64_t)i * m + grp.row0 + lane) * r + k] = s;
   }
 }
 
-// Worker sum and importance from S for rows [row_lo, row_hi); thread per row.
-__global__ void __launch_bounds__(256)
+// Worker sum and importance from S for the rows of groups[0 .. ngroups); one
+// 64-thread block per group, one thread per row.
+__global__ void __launch_bounds__(kWave)
 reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
-                         int64_t m, int32_t N, int32_t r, int64_t row_lo,
-                         int64_t row_hi) {
-  const int64_t p = row_lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= row_hi) return;
+                         const RowGroup* __restrict__ groups, int64_t m, int32_t N,
+                         int32_t r) {
+  const RowGroup grp = groups[blockIdx.x];
+  if ((int32_t)threadIdx.x >= grp.rows) return;
+  const int64_t p = grp.row0 + threadIdx.x;
   float acc = 0.0f;
   if (r == 4) {
     float4 P = *reinterpret_cast<const float4*>(S + p * 4);
@@ -265,81 +267,85 @@ size_t fused_sketch_lds_bytes(int32_t N) {
   return (size_t)N * kTileF4 * sizeof(float4);
 }
 
-hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
-                               const float* g, const float* V, float* S,
-                               float* sigma, int64_t d, int64_t n, int64_t m,
-                               int32_t N, int32_t r, int64_t row_lo,
-                               int64_t row_hi, float eta, float a,
-                               hipStream_t stream) {
-  const int64_t rows = row_hi - row_lo;
-  if (rows <= 0) return hipSuccess;
-  if (N < 1 || N > kMaxFusedWorkers) return hipErrorInvalidValue;
-  const dim3 grid(blocks_for(rows, kWave)), block(N * kWave);
-  const size_t lds = fused_sketch_lds_bytes(N);
-#define ARC_FUSED_CASE(RR)                                                          \
-  case RR:                                                                          \
-    if (grad_bf16)                                                                  \
-      hipLaunchKernelGGL((sketch_fused_kernel<RR, true>), grid, block, lds, stream,  \
-                         grad, h, g, V, S, sigma, d, n, m, row_lo, row_hi, N, eta, a); \
-    else                                                                            \
-      hipLaunchKernelGGL((sketch_fused_kernel<RR, false>), grid, block, lds, stream, \
-                         grad, h, g, V, S, sigma, d, n, m, row_lo, row_hi, N, eta, a); \
-    break;
-  switch (r) {
-    ARC_FUSED_CASE(1)
-    ARC_FUSED_CASE(2)
-    ARC_FUSED_CASE(4)
-    ARC_FUSED_CASE(8)
-    default:
-      return hipErrorInvalidValue;
+namespace {
+
+template <int R, bool BF16>
+struct FusedLaunch {
+  static void run(const void* grad, float* h, const float* g, const float* V,
+                  const RowGroup* groups, int64_t ngroups, float* S, float* sigma,
+                  int64_t d, int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
+    hipLaunchKernelGGL((sketch_fused_kernel<R, BF16>), dim3((unsigned)ngroups),
+                       dim3(N * kWave), fused_sketch_lds_bytes(N), stream, grad, h, g, V,
+                       groups, S, sigma, d, m, N, eta, a);
   }
-#undef ARC_FUSED_CASE
+};
+
+template <int R, bool BF16>
+struct PerWorkerLaunch {
+  static void run(const void* grad, float* h, const float* g, const float* V,
+                  const RowGroup* groups, int64_t ngroups, float* S, int64_t d, int64_t m,
+                  int32_t N, float eta, float a, hipStream_t stream) {
+    hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16>),
+                       dim3(blocks_for(ngroups, kSketchWaves), (unsigned)N),
+                       dim3(kSketchWaves * kWave), 0, stream, grad, h, g, V, groups,
+                       ngroups, S, d, m, eta, a);
+  }
+};
+
+// Launch<r, dtype>::run(args...) for the instantiated r values; false for
+// any other r.
+template <template <int, bool> class Launch, typename... Args>
+bool dispatch_r(int32_t r, bool bf16, Args... args) {
+  switch (r) {
+    case 1: bf16 ? Launch<1, true>::run(args...) : Launch<1, false>::run(args...); return true;
+    case 2: bf16 ? Launch<2, true>::run(args...) : Launch<2, false>::run(args...); return true;
+    case 4: bf16 ? Launch<4, true>::run(args...) : Launch<4, false>::run(args...); return true;
+    case 8: bf16 ? Launch<8, true>::run(args...) : Launch<8, false>::run(args...); return true;
+    default: return false;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
+                               const float* g, const float* V,
+                               const RowGroup* groups, int64_t ngroups,
+                               float* S, float* sigma, int64_t d, int64_t m,
+                               int32_t N, int32_t r, float eta, float a,
+                               hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
+  if (N < 1 || N > kMaxFusedWorkers) return hipErrorInvalidValue;
+  if (!dispatch_r<FusedLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, sigma,
+                               d, m, N, eta, a, stream))
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t launch_sketch(bool fast, const void* grad, int32_t grad_bf16,
-                         float* h, const float* g, const float* V, float* S,
-                         int64_t d, int64_t n, int64_t m, int32_t N, int32_t r,
-                         int64_t row_lo, int64_t row_hi, float eta, float a,
-                         hipStream_t stream) {
-  const int64_t rows = row_hi - row_lo;
-  if (rows <= 0) return hipSuccess;
+                         float* h, const float* g, const float* V,
+                         const RowGroup* groups, int64_t ngroups, float* S,
+                         int64_t d, int64_t m, int32_t N, int32_t r, float eta,
+                         float a, hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
   if (fast) {
-    const dim3 grid(blocks_for(rows, kSketchWaves * kWave), (unsigned)N);
-    const dim3 block(kSketchWaves * kWave);
-#define ARC_SKETCH_CASE(RR)                                                          \
-  case RR:                                                                           \
-    if (grad_bf16)                                                                   \
-      hipLaunchKernelGGL((sketch_per_worker_kernel<RR, true>), grid, block, 0, stream, \
-                         grad, h, g, V, S, d, n, m, row_lo, row_hi, eta, a);         \
-    else                                                                             \
-      hipLaunchKernelGGL((sketch_per_worker_kernel<RR, false>), grid, block, 0,       \
-                         stream, grad, h, g, V, S, d, n, m, row_lo, row_hi, eta, a); \
-    break;
-    switch (r) {
-      ARC_SKETCH_CASE(1)
-      ARC_SKETCH_CASE(2)
-      ARC_SKETCH_CASE(4)
-      ARC_SKETCH_CASE(8)
-      default:
-        return hipErrorInvalidValue;
-    }
-#undef ARC_SKETCH_CASE
+    if (!dispatch_r<PerWorkerLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, d,
+                                     m, N, eta, a, stream))
+      return hipErrorInvalidValue;
   } else {
-    hipLaunchKernelGGL(sketch_generic_kernel, dim3(blocks_for(rows * N, 256)),
-                       dim3(256), 0, stream, grad, grad_bf16, h, g, V, S, d, n,
-                       m, N, r, row_lo, row_hi, eta, a);
+    hipLaunchKernelGGL(sketch_generic_kernel, dim3((unsigned)ngroups, (unsigned)N),
+                       dim3(kWave), 0, stream, grad, grad_bf16, h, g, V, groups, S,
+                       d, m, r, eta, a);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_importance(const float* S, float* sigma, int64_t m,
-                                    int32_t N, int32_t r, int64_t row_lo,
-                                    int64_t row_hi, hipStream_t stream) {
-  const int64_t rows = row_hi - row_lo;
-  if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_importance_kernel, dim3(blocks_for(rows, 256)),
-                     dim3(256), 0, stream, S, sigma, m, N, r, row_lo, row_hi);
+hipError_t launch_reduce_importance(const float* S, float* sigma,
+                                    const RowGroup* groups, int64_t ngroups,
+                                    int64_t m, int32_t N, int32_t r,
+                                    hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_importance_kernel, dim3((unsigned)ngroups), dim3(kWave), 0,
+                     stream, S, sigma, groups, m, N, r);
   return hipGetLastError();
 }
 

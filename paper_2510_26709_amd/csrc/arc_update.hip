@@ -110,6 +110,79 @@ gather_update_generic_kernel(const float* __restrict__ h, float* __restrict__ g,
   agg[tid] = acc;
 }
 
+// ---------------------------------------------------------------------------
+// Per-tensor mode: one work item = one selected row x 4 columns of a tensor.
+// Items are numbered tensor after tensor (GatherBucket::work_off); a thread
+// finds its tensor by binary search.  Same arithmetic as above: for each
+// worker in ascending order Delta = h - g, agg += Delta, g = g + Delta.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+gather_update_tensors_kernel(const float* __restrict__ h, float* __restrict__ g,
+                             const int32_t* __restrict__ idx,
+                             float* __restrict__ agg,
+                             const GatherBucket* __restrict__ buckets,
+                             int32_t nb, int64_t total_work, int64_t d,
+                             int32_t N, int32_t allow_vec) {
+  const int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (w >= total_work) return;
+  int32_t lo = 0, hi = nb;  // last bucket whose work_off <= w
+  while (hi - lo > 1) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (buckets[mid].work_off <= w) lo = mid; else hi = mid;
+  }
+  const GatherBucket bk = buckets[lo];
+  const int64_t per_row = (bk.cols + 3) / 4;
+  const int64_t item = w - bk.work_off;
+  const int64_t q = item / per_row;
+  const int64_t col = (item - q * per_row) * 4;
+  const int64_t p = (int64_t)idx[bk.out_off + q] - bk.row0;
+  float* out = agg + bk.agg_off + q * bk.cols + col;
+  const int64_t ncols = bk.cols - col < 4 ? bk.cols - col : 4;
+  const int64_t e = bk.elem_off + p * bk.cols + col;
+  // Only rows of this tensor; the bounds keep a broken index from touching
+  // memory outside the vectors.
+  if (p < 0 || p >= bk.rows || q >= bk.k || e + ncols > d) return;
+  if (bk.vec && allow_vec) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int32_t i = 0; i < N; ++i) {
+      const int64_t at = (int64_t)i * d + e;
+      const float4 hv = *reinterpret_cast<const float4*>(h + at);
+      const float4 gv = *reinterpret_cast<const float4*>(g + at);
+      float4 dl;
+      dl.x = hv.x - gv.x;
+      dl.y = hv.y - gv.y;
+      dl.z = hv.z - gv.z;
+      dl.w = hv.w - gv.w;
+      if (i == 0) {
+        acc = dl;
+      } else {
+        acc.x = acc.x + dl.x;
+        acc.y = acc.y + dl.y;
+        acc.z = acc.z + dl.z;
+        acc.w = acc.w + dl.w;
+      }
+      float4 gn;
+      gn.x = gv.x + dl.x;
+      gn.y = gv.y + dl.y;
+      gn.z = gv.z + dl.z;
+      gn.w = gv.w + dl.w;
+      *reinterpret_cast<float4*>(g + at) = gn;
+    }
+    *reinterpret_cast<float4*>(out) = acc;
+  } else {
+    for (int64_t jj = 0; jj < ncols; ++jj) {
+      float acc = 0.0f;
+      for (int32_t i = 0; i < N; ++i) {
+        const int64_t at = (int64_t)i * d + e + jj;
+        const float dl = h[at] - g[at];
+        acc = (i == 0) ? dl : acc + dl;
+        g[at] = g[at] + dl;
+      }
+      out[jj] = acc;
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_gather_update(bool fast, const float* h, float* g,
@@ -126,6 +199,18 @@ hipError_t launch_gather_update(bool fast, const float* h, float* g,
                        dim3(blocks_for(K_total * n, 256)), dim3(256), 0, stream,
                        h, g, idx, agg, K_total, d, n, m, N);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_update_tensors(const float* h, float* g,
+                                        const int32_t* idx, float* agg,
+                                        const GatherBucket* buckets, int32_t nb,
+                                        int64_t total_work, int64_t d, int32_t N,
+                                        bool allow_vec, hipStream_t stream) {
+  if (total_work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_update_tensors_kernel, dim3(blocks_for(total_work, 256)),
+                     dim3(256), 0, stream, h, g, idx, agg, buckets, nb, total_work, d, N,
+                     allow_vec ? 1 : 0);
   return hipGetLastError();
 }
 

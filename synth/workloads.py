@@ -10,43 +10,64 @@ involved.
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 
 
-def resnet18_tensors() -> list[int]:
-    """torchvision ResNet-18 (ImageNet head) parameter sizes, in order."""
-    sizes = [64 * 3 * 7 * 7, 64, 64]  # conv1, bn1 weight, bn1 bias
+def resnet18_views() -> list[tuple[int, int]]:
+    """torchvision ResNet-18 (ImageNet head) parameters, in order, as 2-D views:
+    convolution kernels as out x (in*kh*kw), the fc weight as out x in, and
+    1-D tensors (batch-norm weights and biases, fc bias) as one row."""
+    views = [(64, 3 * 7 * 7), (1, 64), (1, 64)]  # conv1, bn1 weight, bn1 bias
     cin = 64
     for cout in (64, 128, 256, 512):
         for block in range(2):
             first_in = cin if block == 0 else cout
-            sizes += [cout * first_in * 9, cout, cout, cout * cout * 9, cout, cout]
+            views += [(cout, first_in * 9), (1, cout), (1, cout), (cout, cout * 9), (1, cout),
+                      (1, cout)]
             if block == 0 and cout != cin:
-                sizes += [cout * cin, cout, cout]  # downsample conv 1x1 + bn
+                views += [(cout, cin), (1, cout), (1, cout)]  # downsample conv 1x1 + bn
         cin = cout
-    sizes += [1000 * 512, 1000]  # fc weight, fc bias
-    return sizes
+    views += [(1000, 512), (1, 1000)]  # fc weight, fc bias
+    return views
+
+
+def gpt2_small_views() -> list[tuple[int, int]]:
+    """GPT-2 small parameters (embeddings, 12 blocks, final LayerNorm) in their
+    stored shapes; the block projections are stored in x out; 1-D tensors as
+    one row."""
+    h = 768
+    views = [(50257, h), (1024, h)]
+    for _ in range(12):
+        views += [(1, h), (1, h), (h, 3 * h), (1, 3 * h), (h, h), (1, h), (1, h), (1, h),
+                  (h, 4 * h), (1, 4 * h), (4 * h, h), (1, h)]
+    views += [(1, h), (1, h)]
+    return views
+
+
+def tinyllama_views() -> list[tuple[int, int]]:
+    """TinyLlama-1.1B: hidden 2048, MLP 5632, 4 KV heads of 64, 22 blocks,
+    untied lm_head; weights out x in, RMSNorm weights as one row."""
+    h, f, kv = 2048, 5632, 256
+    views = [(32000, h)]
+    for _ in range(22):
+        views += [(h, h), (kv, h), (kv, h), (h, h), (f, h), (f, h), (h, f), (1, h), (1, h)]
+    views += [(1, h), (32000, h)]
+    return views
+
+
+def resnet18_tensors() -> list[int]:
+    """ResNet-18 parameter sizes, in order."""
+    return [r * c for r, c in resnet18_views()]
 
 
 def gpt2_small_tensors() -> list[int]:
-    """GPT-2 small parameter sizes (embeddings, 12 blocks, final LayerNorm)."""
-    h = 768
-    sizes = [50257 * h, 1024 * h]
-    for _ in range(12):
-        sizes += [h, h, h * 3 * h, 3 * h, h * h, h, h, h, h * 4 * h, 4 * h, 4 * h * h, h]
-    sizes += [h, h]
-    return sizes
+    """GPT-2 small parameter sizes, in order."""
+    return [r * c for r, c in gpt2_small_views()]
 
 
 def tinyllama_tensors() -> list[int]:
-    """TinyLlama-1.1B layout: hidden 2048, MLP 5632, 4 KV heads of 64, 22 blocks,
-    untied lm_head."""
-    h, f, kv = 2048, 5632, 256
-    sizes = [32000 * h]
-    for _ in range(22):
-        sizes += [h * h, kv * h, kv * h, h * h, f * h, f * h, h * f, h, h]
-    sizes += [h, 32000 * h]
-    return sizes
+    """TinyLlama-1.1B parameter sizes, in order."""
+    return [r * c for r, c in tinyllama_views()]
 
 
 def llama7b_tensors() -> list[int]:
@@ -84,11 +105,24 @@ class Workload:
     boost_frac: float = 0.0
     corr: float = 0.0        # family 1: cross-worker correlation
     buckets_from_tensors: bool = False
+    views: list = field(default_factory=list)  # per-tensor mode: [(rows, cols)]
     description: str = ""
 
     @property
+    def per_tensor(self) -> bool:
+        return bool(self.views)
+
+    @property
     def m(self) -> int:
+        if self.per_tensor:
+            return sum(r for r, _ in self.views)
         return -(-self.d // self.n)
+
+    def tensor_views(self):
+        """Per-tensor mode: [(rows, cols, K)] with K = ceil(mu * rows) for a
+        matrix and the whole tensor for a one-row (1-D) tensor, which the
+        paper's experiments leave uncompressed."""
+        return [(r, c, r if r == 1 else math.ceil(self.mu * r)) for r, c in self.views]
 
     @property
     def bytes_per_grad(self) -> int:
@@ -113,7 +147,9 @@ class Workload:
         return begin, ks
 
     def K_rows(self) -> int:
-        """Selected rows per step (total over buckets)."""
+        """Selected rows per step (total over buckets or tensors)."""
+        if self.per_tensor:
+            return sum(min(k, r) for r, _, k in self.tensor_views())
         b = self.buckets()
         if b is None:
             return min(self.m, math.ceil(self.mu * self.m))
@@ -121,7 +157,15 @@ class Workload:
         return sum(min(k, begin[i + 1] - begin[i]) for i, k in enumerate(ks))
 
     def K_global(self) -> int:
-        return 0 if self.buckets_from_tensors else math.ceil(self.mu * self.m)
+        if self.buckets_from_tensors or self.per_tensor:
+            return 0
+        return math.ceil(self.mu * self.m)
+
+    def payload_elems(self) -> int:
+        """Elements of the aggregated payload per step."""
+        if self.per_tensor:
+            return sum(min(k, r) * c for r, c, k in self.tensor_views())
+        return self.K_rows() * self.n
 
 
 WORKLOADS = {
@@ -156,7 +200,18 @@ WORKLOADS = {
                     "65 norm rows dense), Student-t(3), LogNormal(0,1), corr 0.7, bf16"),
 }
 
+# Per-tensor variants: the same gradients, each tensor compressed in its own
+# 2-D view with its own K (1-D tensors whole).
+for _base, _views in (("resnet18", resnet18_views()), ("gpt2s", gpt2_small_views()),
+                      ("llama1b", tinyllama_views())):
+    _w = WORKLOADS[_base]
+    WORKLOADS[_base + "_tensors"] = replace(
+        _w, name=_base + "_tensors", n=0, views=_views,
+        description=_w.description + "; per-tensor views, K = ceil(mu*rows) per matrix, "
+                                     "1-D tensors whole")
+
 ORDER = ["tiny", "resnet18", "gpt2s", "llama1b", "llama7b"]
+ORDER_TENSORS = ["resnet18_tensors", "gpt2s_tensors", "llama1b_tensors"]
 
 
 def _check_layouts():
@@ -165,6 +220,9 @@ def _check_layouts():
     for name, (count, d) in want.items():
         w = WORKLOADS[name]
         assert len(w.tensors) == count and sum(w.tensors) == d == w.d, name
+    for name in ORDER_TENSORS:
+        w = WORKLOADS[name]
+        assert [r * c for r, c in w.views] == w.tensors, name
 
 
 _check_layouts()

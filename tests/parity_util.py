@@ -67,17 +67,20 @@ def device_buffer(shape, dtype, dev, misalign_floats: int = 0) -> torch.Tensor:
     return base[misalign_floats:].view(*shape)
 
 
-def run_case(*, d, N, n, r=4, K=0, eta=0.1, seed=7, grad_dtype="f32", buckets=None,
-             steps=2, grad_fn=None, data_seed=11, family=0, V=None, misalign=0,
+def run_case(*, d, N, n=0, r=4, K=0, eta=0.1, seed=7, grad_dtype="f32", buckets=None,
+             tensors=None, steps=2, grad_fn=None, data_seed=11, family=0, V=None, misalign=0,
              check_S=False, bit_exact=True, dev="cuda:0", label="case"):
-    """Run `steps` steps of libarctopk and of the oracle from h = g = 0."""
+    """Run `steps` steps of libarctopk and of the oracle from h = g = 0.
+    tensors = [(rows, cols, K), ...] selects the per-tensor mode."""
     dev = torch.device(dev)
     gen = None
     if grad_fn is None:
-        gen = synth.Generator(d, N, data_seed, grad_dtype=grad_dtype, family=family)
+        sizes = None if tensors is None else [a * b for a, b, _ in tensors]
+        gen = synth.Generator(d, N, data_seed, grad_dtype=grad_dtype, family=family,
+                              tensors=sizes)
         grad_fn = gen.fill_host
     comp = arc.Compressor(d=d, N=N, n=n, r=r, K=K, eta=eta, seed=seed, grad_dtype=grad_dtype,
-                          buckets=buckets, device=dev)
+                          buckets=buckets, tensors=tensors, device=dev)
     try:
         if V is not None:
             arc.arc_set_projection(comp.ctx, np.ascontiguousarray(V, dtype=F32))
@@ -96,8 +99,12 @@ def run_case(*, d, N, n, r=4, K=0, eta=0.1, seed=7, grad_dtype="f32", buckets=No
             sigma = comp.sigma()
             S = comp.sketch() if check_S else None
             torch.cuda.synchronize(dev)
-            want = oracle.step(h_o, g_o, grad_np, n=n, r=r, eta=eta, seed=seed, t=t, K=K,
-                               buckets=buckets, V=V, want_sigma=True, want_S=check_S)
+            if tensors is None:
+                want = oracle.step(h_o, g_o, grad_np, n=n, r=r, eta=eta, seed=seed, t=t, K=K,
+                                   buckets=buckets, V=V, want_sigma=True, want_S=check_S)
+            else:
+                want = oracle.step_tensors(h_o, g_o, grad_np, tensors, r=r, eta=eta, seed=seed,
+                                           t=t, want_sigma=True, want_S=check_S)
             got_idx = idx.cpu().numpy()
             assert np.array_equal(got_idx, want["idx"]), \
                 f"{label} t={t}: selected rows differ: {got_idx[:10]} vs {want['idx'][:10]}"

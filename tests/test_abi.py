@@ -111,3 +111,79 @@ def test_binding_raises_with_reason():
     cfg, _ = arc.make_config(**dict(BASE, r=0))
     with pytest.raises(arc.ArcError, match="r must be"):
         arc.arc_create(cfg)
+
+
+def test_tensor_layout_matches_header(tmp_path):
+    src = tmp_path / "tlayout.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "libarctopk.h"\n'
+        'int main(void){printf("%zu %zu %zu %zu", sizeof(arc_tensor),'
+        " offsetof(arc_tensor, rows), offsetof(arc_tensor, cols),"
+        " offsetof(arc_tensor, K));return 0;}\n")
+    exe = tmp_path / "tlayout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals == [ctypes.sizeof(_lib.arc_tensor), _lib.arc_tensor.rows.offset,
+                    _lib.arc_tensor.cols.offset, _lib.arc_tensor.K.offset]
+
+
+TBASE = dict(d=64 * 96 + 300, N=2, r=4, eta=0.1, seed=1,
+             tensors=[(64, 96, 5), (1, 300, 1)])
+
+
+@pytest.mark.parametrize("override", [
+    dict(tensors=[(64, 96, 5), (1, 299, 1)]),      # covers d - 1
+    dict(tensors=[(64, 96, 5), (1, 301, 1)]),      # covers d + 1
+    dict(tensors=[(0, 96, 5), (1, 6444, 1)]),      # empty tensor
+    dict(tensors=[(64, 0, 5), (1, 6444, 1)]),      # zero width
+    dict(tensors=[(64, 96, -1), (1, 300, 1)]),     # negative K
+    dict(n=96),                                    # n with tensors
+    dict(K=3),                                     # global K with tensors
+    dict(buckets=([0, 65], [1])),                  # buckets with tensors
+    dict(reserved2=1),
+    dict(tensors=[(2**40, 2**40, 1)], d=2**40),   # rows*cols would overflow int64
+])
+def test_create_rejects_invalid_tensor_config(override):
+    kw = dict(TBASE, **override)
+    cfg, keep = arc.make_config(**kw)
+    out = ctypes.c_void_p(12345)
+    st = _lib._lib.arc_create(ctypes.byref(cfg), None, ctypes.byref(out))
+    assert st == arc.ARC_ERR_INVALID, arc.arc_last_error()
+    assert out.value is None
+
+
+def test_create_rejects_null_tensor_array():
+    cfg, keep = arc.make_config(**TBASE)
+    cfg.tensors = None
+    assert _lib._lib.arc_create(ctypes.byref(cfg), None,
+                                ctypes.byref(ctypes.c_void_p())) == arc.ARC_ERR_INVALID
+    assert "tensors" in arc.arc_last_error()
+
+
+def test_payload_elems_of_null_context():
+    assert _lib._lib.arc_payload_elems(None) == -1
+
+
+def test_library_projection_matches_oracle_bitwise_on_host():
+    """arc_projection is host code in the library; the oracle generates V from
+    its own SplitMix64 and Box-Muller code.  No device is touched."""
+    import numpy as np
+
+    import oracle
+    for seed, t, n, r in ((2003, 0, 768, 4), (7, 19, 147, 3), (2**64 - 1, 123456, 33, 1),
+                          (0, 5, 1, 32)):
+        got = np.empty((n, r), np.float32)
+        arc.arc_projection(seed, t, n, r, got)
+        want = oracle.projection(seed, t, n, r)
+        assert got.tobytes() == want.tobytes(), (seed, t, n, r)
+
+
+@pytest.mark.parametrize("args", [(1, -1, 4, 4), (1, 0, 0, 4), (1, 0, 4, 0), (1, 0, 4, 33)])
+def test_projection_rejects_bad_arguments(args):
+    import numpy as np
+    buf = np.empty(64, np.float32)
+    with pytest.raises(arc.ArcError):
+        arc.arc_projection(*args, buf)
+    assert _lib._lib.arc_projection(1, 0, 4, 4, None) == arc.ARC_ERR_INVALID

@@ -1,6 +1,6 @@
-"""Full-size parity: the five benchmark workloads at their real sizes, every
-step, in the launch configuration bench.py times, against the CPU oracle run
-on the whole workload.
+"""Full-size parity: the five benchmark workloads at their real sizes, and the
+per-tensor variants of three of them, every step, in the launch configuration
+bench.py times, against the CPU oracle run on the whole workload.
 
 Per step: selected rows and the importance bit-exact; agg bit-exact (and
 within 1e-5 relative max-norm); h and g compared on the selected rows plus a
@@ -35,11 +35,26 @@ def _host_copy(t: torch.Tensor) -> np.ndarray:
     return a.view(np.uint16) if a.dtype == np.int16 else a
 
 
-def _compare_rows(label, dev_state, host_state, rows, n, d):
+def _row_spans(w):
+    """p -> [lo, hi) coordinate range of row p of the workload's view(s)."""
+    if not w.per_tensor:
+        return lambda p: (int(p) * w.n, min(int(p) * w.n + w.n, w.d))
+    rows = np.array([r for r, _ in w.views], np.int64)
+    cols = np.array([c for _, c in w.views], np.int64)
+    row0 = np.concatenate([[0], np.cumsum(rows)])
+    off = np.concatenate([[0], np.cumsum(rows * cols)])
+
+    def span(p):
+        b = int(np.searchsorted(row0, int(p), side="right")) - 1
+        lo = int(off[b] + (int(p) - row0[b]) * cols[b])
+        return lo, lo + int(cols[b])
+    return span
+
+
+def _compare_rows(label, dev_state, host_state, rows, span):
     """Compare the given rows of an [N, d] state (device) with the oracle's."""
-    N = host_state.shape[0]
     for p in rows:
-        lo, hi = int(p) * n, min(int(p) * n + n, d)
+        lo, hi = span(p)
         got = dev_state[:, lo:hi].cpu().numpy()
         compare_float(f"{label} row {p}", got, host_state[:, lo:hi])
 
@@ -60,16 +75,20 @@ def run_workload(name, steps=None, sample_rows=64):
     stream = torch.cuda.current_stream(dev)
     gen = synth.Generator.for_workload(w)
     gdt = torch.int16 if w.grad_dtype == "bf16" else torch.float32
-    log(f"[workload] {name}: d={w.d} N={w.N} n={w.n} m={w.m} grad={w.grad_dtype} steps={steps}")
+    log(f"[workload] {name}: d={w.d} N={w.N} n={w.n} m={w.m} grad={w.grad_dtype} steps={steps}"
+        f"{' tensors=%d' % len(w.views) if w.per_tensor else ''}")
     grad = torch.empty((w.N, w.d), dtype=gdt, device=dev)
     h = torch.zeros((w.N, w.d), dtype=torch.float32, device=dev)
     g = torch.zeros((w.N, w.d), dtype=torch.float32, device=dev)
     h_o = np.zeros((w.N, w.d), F32)
     g_o = np.zeros((w.N, w.d), F32)
     buckets = w.buckets()
+    tensors = w.tensor_views() if w.per_tensor else None
+    span = _row_spans(w)
     comp = arc.Compressor(d=w.d, N=w.N, n=w.n, r=w.r, K=w.K_global(), eta=w.eta,
                           seed=w.sketch_seed, grad_dtype=w.grad_dtype, buckets=buckets,
-                          device=dev, stream=stream)
+                          tensors=tensors, device=dev, stream=stream)
+    log(f"[workload] {name}: {comp.describe()}")
     rng = np.random.default_rng(12345)
     try:
         for t in range(steps):
@@ -81,9 +100,13 @@ def run_workload(name, steps=None, sample_rows=64):
                 sigma = comp.sigma()
                 torch.cuda.synchronize(dev)
             with timed(f"{name} t={t} oracle step ({oracle.num_threads()} threads)"):
-                want = oracle.step(h_o, g_o, grad_np, n=w.n, r=w.r, eta=w.eta,
-                                   seed=w.sketch_seed, t=t, K=w.K_global(), buckets=buckets,
-                                   want_sigma=True)
+                if tensors is None:
+                    want = oracle.step(h_o, g_o, grad_np, n=w.n, r=w.r, eta=w.eta,
+                                       seed=w.sketch_seed, t=t, K=w.K_global(),
+                                       buckets=buckets, want_sigma=True)
+                else:
+                    want = oracle.step_tensors(h_o, g_o, grad_np, tensors, r=w.r, eta=w.eta,
+                                               seed=w.sketch_seed, t=t, want_sigma=True)
             del grad_np
             got_idx = idx.cpu().numpy()
             assert np.array_equal(got_idx, want["idx"]), f"{name} t={t}: selected rows differ"
@@ -94,8 +117,8 @@ def run_workload(name, steps=None, sample_rows=64):
                 got_idx[rng.choice(len(got_idx), size=min(sample_rows, len(got_idx)),
                                    replace=False)] if len(got_idx) else np.zeros(0, int),
                 [w.m - 1]]))
-            _compare_rows(f"{name} t={t} h", h, h_o, rows, w.n, w.d)
-            _compare_rows(f"{name} t={t} g", g, g_o, rows, w.n, w.d)
+            _compare_rows(f"{name} t={t} h", h, h_o, rows, span)
+            _compare_rows(f"{name} t={t} g", g, g_o, rows, span)
             log(f"[workload] {name} t={t}: {len(got_idx)} rows bit-exact; sampled "
                 f"{len(rows)} rows of h, g bit-exact")
         with timed(f"{name} full state compare"):
@@ -124,6 +147,21 @@ def test_workload_gpt2s():
 @pytest.mark.timeout(900)
 def test_workload_llama1b():
     run_workload("llama1b")
+
+
+@pytest.mark.timeout(600)
+def test_workload_resnet18_per_tensor():
+    run_workload("resnet18_tensors")
+
+
+@pytest.mark.timeout(600)
+def test_workload_gpt2s_per_tensor():
+    run_workload("gpt2s_tensors")
+
+
+@pytest.mark.timeout(900)
+def test_workload_llama1b_per_tensor():
+    run_workload("llama1b_tensors", steps=4)
 
 
 @pytest.mark.timeout(1200)
