@@ -551,13 +551,14 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
                                      c->a, c->stream),
             "fused sketch launch");
   } else {
-    ARC_HIP(arc::launch_sketch(true, grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev, nvec,
-                               c->S_dev, c->d, c->m, c->N, c->r, c->eta, c->a, c->stream),
+    ARC_HIP(arc::launch_sketch_per_worker(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev,
+                                          nvec, c->S_dev, c->d, c->m, c->N, c->r, c->eta, c->a,
+                                          c->stream),
             "sketch launch");
   }
-  ARC_HIP(arc::launch_sketch(false, grad, c->grad_bf16, h, g, c->V_dev,
-                             c->groups_dev + nvec, ngroups - nvec, c->S_dev, c->d, c->m, c->N,
-                             c->r, c->eta, c->a, c->stream),
+  ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
+                                     ngroups - nvec, c->S_dev, c->d, c->m, c->N, c->r, c->eta,
+                                     c->a, c->stream),
           "sketch launch (general rows)");
   if ((st = record(c, slot, 2))) return st;
   // Stage 1: worker sum + importance of the rows the fused kernel did not do.

@@ -103,14 +103,20 @@ hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
                                int32_t N, int32_t r, float eta, float a,
                                hipStream_t stream);
 
-// Momentum + residual + per-worker sketch into S for groups[0 .. ngroups).
-// fast: the vectorised per-worker kernel (same requirements as the fused
-// one, any N); otherwise one thread per (row, worker), any group.
-hipError_t launch_sketch(bool fast, const void* grad, int32_t grad_bf16,
-                         float* h, const float* g, const float* V,
-                         const RowGroup* groups, int64_t ngroups, float* S,
-                         int64_t d, int64_t m, int32_t N, int32_t r, float eta,
-                         float a, hipStream_t stream);
+// Momentum + residual + per-worker sketch into S for groups[0 .. ngroups),
+// vectorisable groups (as for the fused kernel), any N.
+hipError_t launch_sketch_per_worker(const void* grad, int32_t grad_bf16, float* h,
+                                    const float* g, const float* V,
+                                    const RowGroup* groups, int64_t ngroups, float* S,
+                                    int64_t d, int64_t m, int32_t N, int32_t r, float eta,
+                                    float a, hipStream_t stream);
+
+// The same for any row group (any width, r <= ARC_MAX_R, element alignment,
+// ragged last row), one wave per (group, worker).
+hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
+                                 const float* g, const float* V, const RowGroup* groups,
+                                 int64_t ngroups, float* S, int64_t d, int64_t m, int32_t N,
+                                 int32_t r, float eta, float a, hipStream_t stream);
 
 // P = sum_i S[i] (ascending i), sigma = row norm squared of P, for the rows
 // of groups[0 .. ngroups).

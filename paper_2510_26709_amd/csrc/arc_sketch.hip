@@ -188,46 +188,6 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   }
 }
 
-// ---------------------------------------------------------------------------
-// General path: one thread per (row, worker) of any row group; any width,
-// d, r and alignment, and ragged tails.  The first pass updates h over the
-// row; then, for each k, one pass re-reads h (new) and g and runs that
-// column's chain.
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kWave)
-sketch_generic_kernel(const void* __restrict__ grad, int32_t grad_bf16,
-                      float* __restrict__ h, const float* __restrict__ g,
-                      const float* __restrict__ V,
-                      const RowGroup* __restrict__ groups, float* __restrict__ S,
-                      int64_t d, int64_t m, int32_t r, float eta, float a) {
-  const RowGroup grp = groups[blockIdx.x];
-  const int lane = threadIdx.x;
-  if (lane >= grp.rows) return;
-  const int32_t i = blockIdx.y;
-  const int64_t n = grp.cols;
-  const int64_t len = lane == grp.rows - 1 ? grp.last_len : n;
-  const int64_t base = (int64_t)i * d + grp.elem_off + lane * n;
-  const float* Vg = V + grp.v_off;
-  for (int64_t j = 0; j < len; ++j) {
-    const int64_t e = base + j;
-    float x;
-    if (grad_bf16)
-      x = __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e] << 16);
-    else
-      x = static_cast<const float*>(grad)[e];
-    h[e] = fmaf(eta, x, a * h[e]);
-  }
-  for (int32_t k = 0; k < r; ++k) {
-    float s = 0.0f;
-    for (int64_t j = 0; j < len; ++j) {
-      const int64_t e = base + j;
-      const float dl = h[e] - g[e];
-      s = fmaf(dl, Vg[j * r + k], s);
-    }
-    S[((int64_t)i * m + grp.row0 + lane) * r + k] = s;
-  }
-}
-
 // Worker sum and importance from S for the rows of groups[0 .. ngroups); one
 // 64-thread block per group, one thread per row.
 __global__ void __launch_bounds__(kWave)
@@ -321,21 +281,15 @@ hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
   return hipGetLastError();
 }
 
-hipError_t launch_sketch(bool fast, const void* grad, int32_t grad_bf16,
-                         float* h, const float* g, const float* V,
-                         const RowGroup* groups, int64_t ngroups, float* S,
-                         int64_t d, int64_t m, int32_t N, int32_t r, float eta,
-                         float a, hipStream_t stream) {
+hipError_t launch_sketch_per_worker(const void* grad, int32_t grad_bf16, float* h,
+                                    const float* g, const float* V,
+                                    const RowGroup* groups, int64_t ngroups, float* S,
+                                    int64_t d, int64_t m, int32_t N, int32_t r, float eta,
+                                    float a, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
-  if (fast) {
-    if (!dispatch_r<PerWorkerLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, d,
-                                     m, N, eta, a, stream))
-      return hipErrorInvalidValue;
-  } else {
-    hipLaunchKernelGGL(sketch_generic_kernel, dim3((unsigned)ngroups, (unsigned)N),
-                       dim3(kWave), 0, stream, grad, grad_bf16, h, g, V, groups, S,
-                       d, m, r, eta, a);
-  }
+  if (!dispatch_r<PerWorkerLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, d, m,
+                                   N, eta, a, stream))
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

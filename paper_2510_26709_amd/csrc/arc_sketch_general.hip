@@ -1,0 +1,110 @@
+// General sketch kernel: the same streaming stage as the vectorised kernels
+// (EF21M momentum (11a), Delta = h_t - g_{t-1}, per-worker sketch of Alg. 1)
+// for row groups the 16-byte kernels cannot take: any row width, any r up to
+// ARC_MAX_R, element-aligned pointers, and a ragged last row.
+//
+// One wave per (row group, worker).  Each 32-column chunk of the group's
+// 64 x 32 tile is loaded with one element per lane (two rows of 32 columns
+// per instruction, coalesced), 24 loads in flight per pass of 16 rows; Delta
+// goes to LDS, then lane p runs its row's r chains over the chunk in
+// ascending column order, its partial sums kept in LDS between chunks.  The
+// arithmetic is the same as the vectorised kernels', in the same order, so
+// both produce the same bits.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "arc_device.h"
+#include "arc_internal.h"
+#include "libarctopk.h"
+
+namespace arc {
+namespace {
+
+constexpr int kGenChunk = 32;       // columns per chunk
+constexpr int kGenPitch = kGenChunk + 1;  // LDS row pitch (floats), conflict-free row reads
+constexpr int kGenRowsPerPass = 16;  // rows loaded per pass: 8 instructions x 2 rows
+
+__global__ void __launch_bounds__(kWave)
+sketch_general_kernel(const void* __restrict__ grad, int32_t grad_bf16,
+                      float* __restrict__ h, const float* __restrict__ g,
+                      const float* __restrict__ V,
+                      const RowGroup* __restrict__ groups, float* __restrict__ S,
+                      int64_t d, int64_t m, int32_t r, float eta, float a) {
+  __shared__ float tile[kWave * kGenPitch];
+  extern __shared__ float acc[];  // [r][64] partial sums
+  const RowGroup grp = groups[blockIdx.x];
+  const int lane = threadIdx.x;
+  const int32_t i = blockIdx.y;
+  const int64_t n = grp.cols;
+  const int32_t rows = grp.rows;
+  const int64_t base = (int64_t)i * d + grp.elem_off;
+  const float* Vg = V + grp.v_off;
+  const int half = lane >> 5;            // row of the pair this lane loads
+  const int cl = lane & (kGenChunk - 1);  // column within the chunk
+  for (int32_t k = 0; k < r; ++k) acc[k * kWave + lane] = 0.0f;
+
+  for (int64_t c0 = 0; c0 < n; c0 += kGenChunk) {
+    const int cw = (int)(n - c0 < kGenChunk ? n - c0 : kGenChunk);
+    for (int pass = 0; pass * kGenRowsPerPass < rows; ++pass) {
+      float xv[8], hv[8], gv[8];
+      bool ok[8];
+      int64_t e[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int l = pass * kGenRowsPerPass + u * 2 + half;
+        const int64_t len = l == rows - 1 ? grp.last_len : n;
+        ok[u] = l < rows && cl < cw && c0 + cl < len;
+        e[u] = base + (int64_t)l * n + c0 + cl;
+        xv[u] = hv[u] = gv[u] = 0.0f;
+        if (ok[u]) {
+          xv[u] = grad_bf16
+                      ? __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e[u]] << 16)
+                      : static_cast<const float*>(grad)[e[u]];
+          hv[u] = h[e[u]];
+          gv[u] = g[e[u]];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int l = pass * kGenRowsPerPass + u * 2 + half;
+        const float hn = fmaf(eta, xv[u], a * hv[u]);
+        if (ok[u]) h[e[u]] = hn;
+        tile[l * kGenPitch + cl] = hn - gv[u];
+      }
+    }
+    wave_lds_fence();
+    if (lane < rows) {
+      // this row's columns in the chunk (fewer in a ragged last row)
+      const int64_t len = lane == rows - 1 ? grp.last_len : n;
+      const int jn = (int)(len - c0 < cw ? (len - c0 > 0 ? len - c0 : 0) : cw);
+      const float* row = tile + lane * kGenPitch;
+      const float* Vc = Vg + c0 * r;
+      for (int32_t k = 0; k < r; ++k) {
+        float s = acc[k * kWave + lane];
+        for (int j = 0; j < jn; ++j) s = fmaf(row[j], Vc[j * r + k], s);
+        acc[k * kWave + lane] = s;
+      }
+    }
+    wave_lds_fence();
+  }
+  if (lane < rows) {
+    float* out = S + ((int64_t)i * m + grp.row0 + lane) * r;
+    for (int32_t k = 0; k < r; ++k) out[k] = acc[k * kWave + lane];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
+                                 const float* g, const float* V, const RowGroup* groups,
+                                 int64_t ngroups, float* S, int64_t d, int64_t m, int32_t N,
+                                 int32_t r, float eta, float a, hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
+  if (r < 1 || r > ARC_MAX_R) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sketch_general_kernel, dim3((unsigned)ngroups, (unsigned)N), dim3(kWave),
+                     sizeof(float) * kWave * r, stream, grad, grad_bf16, h, g, V, groups, S, d,
+                     m, r, eta, a);
+  return hipGetLastError();
+}
+
+}  // namespace arc

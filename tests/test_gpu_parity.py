@@ -50,6 +50,11 @@ CASES = [
     ("bf16_fused_r8_N2", dict(d=64 * 3000, N=2, n=64, r=8, K=40, steps=2, grad_dtype="bf16",
                               family=1)),
     ("select_many_blocks", dict(d=32 * 300_000, N=1, n=32, r=4, K=150_000, steps=1)),
+    ("generic_r32_max", dict(d=40 * 500 + 13, N=3, n=40, r=32, K=7, steps=2)),
+    ("generic_r17_bf16", dict(d=72 * 300 + 5, N=2, n=72, r=17, K=9, steps=2, grad_dtype="bf16",
+                              family=1)),
+    ("generic_wide_ragged", dict(d=1000 * 70 + 999, N=3, n=1000, r=4, K=5, steps=2)),
+    ("generic_many_workers", dict(d=50 * 257, N=11, n=50, r=4, K=20, steps=2)),
 ]
 
 
