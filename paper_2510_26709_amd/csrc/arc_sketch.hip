@@ -59,17 +59,24 @@ __device__ __forceinline__ void sketch_rows(
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
 
   const uint32_t nchunks = n / kChunk;
+  uint2 x_next[8];  // bf16: this lane's grad of the next chunk
   for (uint32_t c = 0; c < nchunks; ++c) {
     float4 xv[8], hv[8], gv[8];
+    const bool even = (c & 1) == 0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if constexpr (BF16) {
-        // 8-byte loads cover half a cache line whose other half belongs to
-        // the next chunk, so these stay cacheable.  (Counters show about half
-        // of those lines leave L2 twice; the second request is served by the
-        // last-level cache.  Loading both halves together removes it but
-        // costs occupancy and runs no faster.)
-        const uint2 w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
+        // A row's bf16 grad for two consecutive chunks is one 128-byte line;
+        // both 8-byte halves are requested together on even chunks, so the
+        // line is fetched once rather than once per chunk.
+        uint2 w;
+        if (even) {
+          w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
+          if (c + 1 < nchunks)
+            x_next[u] = buffer_load_u2<kCacheDefault>(rx, off[u] / 2 + kChunk * 2);
+        } else {
+          w = x_next[u];
+        }
         xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
       } else {
         xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, off[u]);
@@ -77,7 +84,7 @@ __device__ __forceinline__ void sketch_rows(
       hv[u] = buffer_load_f4<kCacheDefault>(rh, off[u]);
       gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, off[u]);
     }
-    // Keep all 24 loads of the chunk in flight before the first use.
+    // Keep all loads of the chunk in flight before the first use.
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
