@@ -50,7 +50,7 @@ struct BucketState {
 };
 
 // A group of up to 64 consecutive rows of one view (one wave's rows in the
-// sketch kernels).  Rows are `cols` wide and start `elem_off` coordinates into
+// sketch kernels; the vectorised kernels take groups of 64, 32 or 16 rows).  Rows are `cols` wide and start `elem_off` coordinates into
 // each worker's vector; their projection is V[v_off .. v_off + cols*r).
 struct RowGroup {
   int64_t elem_off;  // coordinate of the group's first element
@@ -92,11 +92,17 @@ struct SelectWorkspace {
 // Bytes of LDS one block of the fused sketch kernel uses for N workers.
 size_t fused_sketch_lds_bytes(int32_t N);
 
+// Row groups of group_rows rows take chunks of vector_chunk_cols(group_rows)
+// columns in the vectorised sketch kernels.
+constexpr int32_t vector_chunk_cols(int32_t group_rows) { return 2048 / group_rows; }
+
 // Momentum + residual + per-worker sketch + worker sum + importance for the
 // row groups groups[0 .. ngroups): one block per group holding all N <= 8
-// workers.  Every group must be vectorisable (cols % 32 == 0, 16-byte aligned
-// rows, r in {1,2,4,8}, no ragged tail, rows*cols*4 < 2^31).
-hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
+// workers.  Every group must be vectorisable for group_rows in {64, 32, 16}:
+// at most group_rows rows, cols a multiple of vector_chunk_cols(group_rows),
+// 16-byte aligned rows, r in {1,2,4,8}, no ragged tail, rows*cols*4 < 2^31.
+hipError_t launch_sketch_fused(int32_t group_rows, const void* grad, int32_t grad_bf16,
+                               float* h,
                                const float* g, const float* V,
                                const RowGroup* groups, int64_t ngroups,
                                float* S, float* sigma, int64_t d, int64_t m,
@@ -105,8 +111,8 @@ hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
 
 // Momentum + residual + per-worker sketch into S for groups[0 .. ngroups),
 // vectorisable groups (as for the fused kernel), any N.
-hipError_t launch_sketch_per_worker(const void* grad, int32_t grad_bf16, float* h,
-                                    const float* g, const float* V,
+hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_t grad_bf16,
+                                    float* h, const float* g, const float* V,
                                     const RowGroup* groups, int64_t ngroups, float* S,
                                     int64_t d, int64_t m, int32_t N, int32_t r, float eta,
                                     float a, hipStream_t stream);

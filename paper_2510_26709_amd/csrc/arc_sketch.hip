@@ -15,32 +15,44 @@
 namespace arc {
 namespace {
 
-// Tile of one wave: 64 rows x 32 columns of Delta, 8 float4 per row plus one
-// float4 of padding, so that 16 consecutive lanes reading 16 consecutive rows
-// hit 16 distinct 16-byte bank groups; every address is a per-lane base plus
-// an immediate offset.
-constexpr int kChunk = 32;
-constexpr int kRowF4 = 9;
-constexpr int kTileF4 = kWave * kRowF4;
-__device__ __forceinline__ int tile_slot(int rho, int q) { return rho * kRowF4 + q; }
+// Row groups of G in {64, 32, 16} rows.  One 16-byte load instruction of a
+// wave covers G/8 rows of LPR = 512/G lanes each, so eight instructions cover
+// the group's G rows over a chunk of CW = 4*LPR columns (32, 64 or 128).  The
+// LDS tile holds G rows of Delta with LPR float4 per row plus one float4 of
+// padding (at most 576 float4 for every G), so that consecutive lanes reading
+// consecutive rows hit distinct 16-byte bank groups.
+template <int G>
+struct GroupShape {
+  static_assert(G == 64 || G == 32 || G == 16, "row group of 64, 32 or 16 rows");
+  static constexpr int kLanesPerRow = 512 / G;
+  static constexpr int kRowsPerLoad = kWave / kLanesPerRow;
+  static constexpr int kChunkCols = 4 * kLanesPerRow;
+  static constexpr int kRowF4 = kLanesPerRow + 1;
+};
+constexpr int kTileF4 = 576;  // >= G * (512 / G + 1) for every G
 
 // One wave's pass over the rows of one row group of worker i: loads the
-// grad/h/g tile of each 32-column chunk with coalesced 16-byte accesses,
-// applies (11a), writes h back, parks Delta in LDS, then runs this lane's r
-// chains over its row.  Local row l of the group starts at coordinate
-// elem_off + l*n.  The three streams are read through buffer resources that
-// end at the group's last row, so in a group of fewer than 64 rows the
-// missing rows read as zero (their lanes' sketches are discarded by the
-// caller) and are not stored.
-template <int R, bool BF16>
+// grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
+// writes h back, parks Delta in LDS, then runs this lane's r chains over its
+// row.  Local row l of the group starts at coordinate elem_off + l*n.  The
+// three streams are read through buffer resources that end at the group's
+// last row, so in a group of fewer than G rows the missing rows read as zero
+// and are not stored.  Lanes G..63 repeat the chains of lanes 0..G-1; the
+// caller keeps only lanes below the group's row count.
+template <int R, bool BF16, int G>
 __device__ __forceinline__ void sketch_rows(
     const void* __restrict__ grad, float* __restrict__ h,
     const float* __restrict__ g, const float* __restrict__ V, int64_t d,
     const RowGroup& grp, int32_t i, float eta, float a, float4* tile,
     float (&s)[R]) {
+  using Shape = GroupShape<G>;
+  constexpr int kLPR = Shape::kLanesPerRow;
+  constexpr int kRPL = Shape::kRowsPerLoad;
+  constexpr int kCW = Shape::kChunkCols;
+  constexpr int kPitch = Shape::kRowF4;
   const int lane = threadIdx.x & (kWave - 1);
-  const int sub = lane >> 3;   // row within an 8-row slab
-  const int quad = lane & 7;   // 16-byte column group within the chunk
+  const int sub = lane / kLPR;   // row within one load's rows
+  const int quad = lane % kLPR;  // 16-byte column group within the chunk
   const uint32_t n = (uint32_t)grp.cols;
   const int32_t rows = grp.rows;
   const int64_t wbase = (int64_t)i * d + grp.elem_off;
@@ -51,32 +63,36 @@ __device__ __forceinline__ void sketch_rows(
       BF16 ? make_buffer(static_cast<const uint16_t*>(grad) + wbase, bytes / 2)
            : make_buffer(static_cast<const float*>(grad) + wbase, bytes);
   V += grp.v_off;
-  // byte offset of this lane's 16 bytes of binary32 in row u*8 + sub
+  // byte offset of this lane's 16 bytes of binary32 in row u*kRPL + sub
   uint32_t off[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * 8 + sub) * n + quad * 4) * 4u;
+  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * kRPL + sub) * n + quad * 4) * 4u;
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
 
-  const uint32_t nchunks = n / kChunk;
-  uint2 x_next[8];  // bf16: this lane's grad of the next chunk
+  const uint32_t nchunks = n / kCW;
+  uint2 x_next[8];  // bf16, 64-row groups: this lane's grad of the next chunk
   for (uint32_t c = 0; c < nchunks; ++c) {
     float4 xv[8], hv[8], gv[8];
     const bool even = (c & 1) == 0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      if constexpr (BF16) {
-        // A row's bf16 grad for two consecutive chunks is one 128-byte line;
-        // both 8-byte halves are requested together on even chunks, so the
-        // line is fetched once rather than once per chunk.
+      if constexpr (BF16 && G == 64) {
+        // A row's bf16 grad for two consecutive 32-column chunks is one
+        // 128-byte line; both 8-byte halves are requested together on even
+        // chunks, so the line is fetched once rather than once per chunk.
         uint2 w;
         if (even) {
           w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
           if (c + 1 < nchunks)
-            x_next[u] = buffer_load_u2<kCacheDefault>(rx, off[u] / 2 + kChunk * 2);
+            x_next[u] = buffer_load_u2<kCacheDefault>(rx, off[u] / 2 + kCW * 2);
         } else {
           w = x_next[u];
         }
+        xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
+      } else if constexpr (BF16) {
+        // 32 or more lanes per row: each load already covers whole lines.
+        const uint2 w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
         xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
       } else {
         xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, off[u]);
@@ -93,20 +109,21 @@ __device__ __forceinline__ void sketch_rows(
       hn.y = fmaf(eta, xv[u].y, a * hv[u].y);
       hn.z = fmaf(eta, xv[u].z, a * hv[u].z);
       hn.w = fmaf(eta, xv[u].w, a * hv[u].w);
-      if (u * 8 + sub < rows) buffer_store_f4<kCacheNonTemporal>(rh, off[u], hn);
+      if (u * kRPL + sub < rows) buffer_store_f4<kCacheNonTemporal>(rh, off[u], hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
       dl.z = hn.z - gv[u].z;
       dl.w = hn.w - gv[u].w;
-      tile[tile_slot(u * 8 + sub, quad)] = dl;
-      off[u] += kChunk * 4;
+      tile[(u * kRPL + sub) * kPitch + quad] = dl;
+      off[u] += kCW * 4;
     }
     wave_lds_fence();
-    const float* Vc = V + c * kChunk * R;
+    const float* Vc = V + c * kCW * R;
+    const float4* my_row = tile + (lane & (G - 1)) * kPitch;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const float4 dv = tile[tile_slot(lane, q)];
+    for (int q = 0; q < kLPR; ++q) {
+      const float4 dv = my_row[q];
       const float e4[4] = {dv.x, dv.y, dv.z, dv.w};
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
@@ -120,14 +137,14 @@ __device__ __forceinline__ void sketch_rows(
 }
 
 // ---------------------------------------------------------------------------
-// Fused path: a block is N waves, wave i streams worker i over the same 64
-// rows; the waves then meet in LDS and wave 0 forms P = S^(0) + S^(1) + ...
-// (ascending worker order) and Sigma for its 64 rows.  Sketches never leave
+// Fused path: a block is N waves, wave i streams worker i over the same row
+// group; the waves then meet in LDS and wave 0 forms P = S^(0) + S^(1) + ...
+// (ascending worker order) and Sigma for the group's rows.  Sketches never leave
 // the chip except as the per-worker copy S kept for inspection.
 // HBM traffic per element and worker: grad (4 or 2 B) + h read and write
 // (8 B) + g read (4 B).
 // ---------------------------------------------------------------------------
-template <int R, bool BF16>
+template <int R, bool BF16, int G>
 __global__ void __launch_bounds__(kMaxFusedWorkers * kWave)
 sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
                     const float* __restrict__ g, const float* __restrict__ V,
@@ -140,7 +157,7 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
   const RowGroup grp = groups[xcd_contiguous_block(blockIdx.x, gridDim.x)];
   float4* tile = lds_tiles + i * kTileF4;
   float s[R];
-  sketch_rows<R, BF16>(grad, h, g, V, d, grp, i, eta, a, tile, s);
+  sketch_rows<R, BF16, G>(grad, h, g, V, d, grp, i, eta, a, tile, s);
   const bool mine = lane < grp.rows;
   const int64_t p = grp.row0 + lane;
   if (mine) {
@@ -168,11 +185,11 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
 
 // ---------------------------------------------------------------------------
 // Per-worker path (more workers than one block holds): same streaming, one
-// wave per (64 rows, worker), sketch written to S for the reduce kernel.
+// wave per (row group, worker), sketch written to S for the reduce kernel.
 // ---------------------------------------------------------------------------
 constexpr int kSketchWaves = 4;
 
-template <int R, bool BF16>
+template <int R, bool BF16, int G>
 __global__ void __launch_bounds__(kSketchWaves * kWave)
 sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
                          const float* __restrict__ g, const float* __restrict__ V,
@@ -187,7 +204,7 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   if (gi >= ngroups) return;  // whole wave; no block barrier follows
   const RowGroup grp = groups[gi];
   float s[R];
-  sketch_rows<R, BF16>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
+  sketch_rows<R, BF16, G>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
   if (lane < grp.rows) {
     float* out = S + ((int64_t)i * m + grp.row0 + lane) * R;
 #pragma unroll
@@ -236,66 +253,80 @@ size_t fused_sketch_lds_bytes(int32_t N) {
 
 namespace {
 
-template <int R, bool BF16>
+template <int R, bool BF16, int G>
 struct FusedLaunch {
   static void run(const void* grad, float* h, const float* g, const float* V,
                   const RowGroup* groups, int64_t ngroups, float* S, float* sigma,
                   int64_t d, int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
-    hipLaunchKernelGGL((sketch_fused_kernel<R, BF16>), dim3((unsigned)ngroups),
+    hipLaunchKernelGGL((sketch_fused_kernel<R, BF16, G>), dim3((unsigned)ngroups),
                        dim3(N * kWave), fused_sketch_lds_bytes(N), stream, grad, h, g, V,
                        groups, S, sigma, d, m, N, eta, a);
   }
 };
 
-template <int R, bool BF16>
+template <int R, bool BF16, int G>
 struct PerWorkerLaunch {
   static void run(const void* grad, float* h, const float* g, const float* V,
                   const RowGroup* groups, int64_t ngroups, float* S, int64_t d, int64_t m,
                   int32_t N, float eta, float a, hipStream_t stream) {
-    hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16>),
+    hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16, G>),
                        dim3(blocks_for(ngroups, kSketchWaves), (unsigned)N),
                        dim3(kSketchWaves * kWave), 0, stream, grad, h, g, V, groups,
                        ngroups, S, d, m, eta, a);
   }
 };
 
-// Launch<r, dtype>::run(args...) for the instantiated r values; false for
-// any other r.
-template <template <int, bool> class Launch, typename... Args>
-bool dispatch_r(int32_t r, bool bf16, Args... args) {
+template <template <int, bool, int> class Launch, int R, bool BF16, typename... Args>
+bool dispatch_g(int32_t group_rows, Args... args) {
+  switch (group_rows) {
+    case 64: Launch<R, BF16, 64>::run(args...); return true;
+    case 32: Launch<R, BF16, 32>::run(args...); return true;
+    case 16: Launch<R, BF16, 16>::run(args...); return true;
+    default: return false;
+  }
+}
+
+// Launch<r, dtype, group_rows>::run(args...) for the instantiated values;
+// false for any other r or group size.
+template <template <int, bool, int> class Launch, typename... Args>
+bool dispatch(int32_t r, bool bf16, int32_t group_rows, Args... args) {
   switch (r) {
-    case 1: bf16 ? Launch<1, true>::run(args...) : Launch<1, false>::run(args...); return true;
-    case 2: bf16 ? Launch<2, true>::run(args...) : Launch<2, false>::run(args...); return true;
-    case 4: bf16 ? Launch<4, true>::run(args...) : Launch<4, false>::run(args...); return true;
-    case 8: bf16 ? Launch<8, true>::run(args...) : Launch<8, false>::run(args...); return true;
+    case 1: return bf16 ? dispatch_g<Launch, 1, true>(group_rows, args...)
+                        : dispatch_g<Launch, 1, false>(group_rows, args...);
+    case 2: return bf16 ? dispatch_g<Launch, 2, true>(group_rows, args...)
+                        : dispatch_g<Launch, 2, false>(group_rows, args...);
+    case 4: return bf16 ? dispatch_g<Launch, 4, true>(group_rows, args...)
+                        : dispatch_g<Launch, 4, false>(group_rows, args...);
+    case 8: return bf16 ? dispatch_g<Launch, 8, true>(group_rows, args...)
+                        : dispatch_g<Launch, 8, false>(group_rows, args...);
     default: return false;
   }
 }
 
 }  // namespace
 
-hipError_t launch_sketch_fused(const void* grad, int32_t grad_bf16, float* h,
-                               const float* g, const float* V,
+hipError_t launch_sketch_fused(int32_t group_rows, const void* grad, int32_t grad_bf16,
+                               float* h, const float* g, const float* V,
                                const RowGroup* groups, int64_t ngroups,
                                float* S, float* sigma, int64_t d, int64_t m,
                                int32_t N, int32_t r, float eta, float a,
                                hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
   if (N < 1 || N > kMaxFusedWorkers) return hipErrorInvalidValue;
-  if (!dispatch_r<FusedLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, sigma,
-                               d, m, N, eta, a, stream))
+  if (!dispatch<FusedLaunch>(r, grad_bf16 != 0, group_rows, grad, h, g, V, groups, ngroups, S,
+                             sigma, d, m, N, eta, a, stream))
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_sketch_per_worker(const void* grad, int32_t grad_bf16, float* h,
-                                    const float* g, const float* V,
+hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_t grad_bf16,
+                                    float* h, const float* g, const float* V,
                                     const RowGroup* groups, int64_t ngroups, float* S,
                                     int64_t d, int64_t m, int32_t N, int32_t r, float eta,
                                     float a, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
-  if (!dispatch_r<PerWorkerLaunch>(r, grad_bf16 != 0, grad, h, g, V, groups, ngroups, S, d, m,
-                                   N, eta, a, stream))
+  if (!dispatch<PerWorkerLaunch>(r, grad_bf16 != 0, group_rows, grad, h, g, V, groups,
+                                 ngroups, S, d, m, N, eta, a, stream))
     return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -24,10 +24,10 @@ constexpr int kGenChunk = 32;       // columns per chunk
 constexpr int kGenPitch = kGenChunk + 1;  // LDS row pitch (floats), conflict-free row reads
 constexpr int kGenRowsPerPass = 16;  // rows loaded per pass: 8 instructions x 2 rows
 
+template <bool BF16>
 __global__ void __launch_bounds__(kWave)
-sketch_general_kernel(const void* __restrict__ grad, int32_t grad_bf16,
-                      float* __restrict__ h, const float* __restrict__ g,
-                      const float* __restrict__ V,
+sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
+                      const float* __restrict__ g, const float* __restrict__ V,
                       const RowGroup* __restrict__ groups, float* __restrict__ S,
                       int64_t d, int64_t m, int32_t r, float eta, float a) {
   __shared__ float tile[kWave * kGenPitch];
@@ -49,20 +49,20 @@ sketch_general_kernel(const void* __restrict__ grad, int32_t grad_bf16,
       float xv[8], hv[8], gv[8];
       bool ok[8];
       int64_t e[8];
+      // Every lane loads; a lane without an element of the group loads the
+      // group's first element instead (always present) and discards it.
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int l = pass * kGenRowsPerPass + u * 2 + half;
         const int64_t len = l == rows - 1 ? grp.last_len : n;
         ok[u] = l < rows && cl < cw && c0 + cl < len;
-        e[u] = base + (int64_t)l * n + c0 + cl;
-        xv[u] = hv[u] = gv[u] = 0.0f;
-        if (ok[u]) {
-          xv[u] = grad_bf16
-                      ? __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e[u]] << 16)
-                      : static_cast<const float*>(grad)[e[u]];
-          hv[u] = h[e[u]];
-          gv[u] = g[e[u]];
-        }
+        e[u] = ok[u] ? base + (int64_t)l * n + c0 + cl : base;
+        if constexpr (BF16)
+          xv[u] = __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e[u]] << 16);
+        else
+          xv[u] = static_cast<const float*>(grad)[e[u]];
+        hv[u] = h[e[u]];
+        gv[u] = g[e[u]];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -73,15 +73,22 @@ sketch_general_kernel(const void* __restrict__ grad, int32_t grad_bf16,
       }
     }
     wave_lds_fence();
-    if (lane < rows) {
-      // this row's columns in the chunk (fewer in a ragged last row)
+    {
+      // This row's columns in the chunk: fewer in a ragged last row.  The
+      // column loop runs to the chunk width for every lane, so that V is
+      // read as wave-uniform scalars; the lane keeps only its first jn
+      // products.  Lanes at or past the row count compute unused values.
       const int64_t len = lane == rows - 1 ? grp.last_len : n;
       const int jn = (int)(len - c0 < cw ? (len - c0 > 0 ? len - c0 : 0) : cw);
       const float* row = tile + lane * kGenPitch;
       const float* Vc = Vg + c0 * r;
       for (int32_t k = 0; k < r; ++k) {
         float s = acc[k * kWave + lane];
-        for (int j = 0; j < jn; ++j) s = fmaf(row[j], Vc[j * r + k], s);
+#pragma unroll 8
+        for (int j = 0; j < cw; ++j) {
+          const float t = fmaf(row[j], Vc[j * r + k], s);
+          s = j < jn ? t : s;
+        }
         acc[k * kWave + lane] = s;
       }
     }
@@ -101,9 +108,14 @@ hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
                                  int32_t r, float eta, float a, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
   if (r < 1 || r > ARC_MAX_R) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(sketch_general_kernel, dim3((unsigned)ngroups, (unsigned)N), dim3(kWave),
-                     sizeof(float) * kWave * r, stream, grad, grad_bf16, h, g, V, groups, S, d,
-                     m, r, eta, a);
+  const dim3 grid((unsigned)ngroups, (unsigned)N), block(kWave);
+  const size_t lds = sizeof(float) * kWave * r;
+  if (grad_bf16)
+    hipLaunchKernelGGL(sketch_general_kernel<true>, grid, block, lds, stream, grad, h, g, V,
+                       groups, S, d, m, r, eta, a);
+  else
+    hipLaunchKernelGGL(sketch_general_kernel<false>, grid, block, lds, stream, grad, h, g, V,
+                       groups, S, d, m, r, eta, a);
   return hipGetLastError();
 }
 
