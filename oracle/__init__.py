@@ -44,6 +44,11 @@ def _load():
         "oracle_step_tensors": (ctypes.c_int, [_i32, _i32, _f32, _u64, _i64, _i32, _vp, _vp, _vp,
                                                _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                                _vp]),
+        "oracle_dense_step": (ctypes.c_int, [_i32, _i64, _f32, _vp, _i32, _vp, _vp, _vp]),
+        "oracle_accumulate_rows": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp]),
+        "oracle_accumulate_tensors": (ctypes.c_int, [_i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "oracle_optimizer": (ctypes.c_int, [_i32, _i32, _i64, _i64, _f32, _f32, _f32, _f32, _f32,
+                                            _f32, _vp, _vp, _vp, _vp]),
         "oracle_num_threads": (ctypes.c_int, []),
     }
     for name, (res, args) in sig.items():
@@ -248,3 +253,48 @@ def step_tensors(h: np.ndarray, g: np.ndarray, grad: np.ndarray, tensors, *, r: 
     if want_S:
         out["S"] = S
     return out
+
+
+# ---- model step around the compressor (Eq. (11c), optimisers, warm-up) ----
+
+OPTIMIZERS = {"sgd": 0, "msgd": 1, "adam": 2}
+
+
+def dense_step(h: np.ndarray, g: np.ndarray, G: np.ndarray, grad: np.ndarray, eta: float) -> None:
+    """Identity-compressor step in place: (11a), (11b) with C = I, G += payload."""
+    _f32c(h, "h"), _f32c(g, "g"), _f32c(G, "G")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    N, d = h.shape
+    if g.shape != h.shape or grad.shape != h.shape or G.shape != (d,):
+        raise ValueError("h, g, grad must be [N, d]; G must be [d]")
+    _check(_load().oracle_dense_step(N, d, eta, _ptr(grad), is_bf16, _ptr(h), _ptr(g), _ptr(G)),
+           "dense_step")
+
+
+def accumulate(G: np.ndarray, idx: np.ndarray, agg: np.ndarray, *, n: int = 0,
+               tensors=None) -> None:
+    """G += agg at the selected rows (single view of width n, or tensors)."""
+    _f32c(G, "G")
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    agg = np.ascontiguousarray(agg, dtype=np.float32).reshape(-1)
+    if tensors is None:
+        _check(_load().oracle_accumulate_rows(G.shape[0], n, idx.shape[0], _ptr(idx), _ptr(agg),
+                                              _ptr(G)), "accumulate")
+    else:
+        tens = np.asarray(tensors, dtype=np.int64).reshape(-1, 3)
+        rows, cols, ks = (np.ascontiguousarray(tens[:, c]) for c in range(3))
+        _check(_load().oracle_accumulate_tensors(len(rows), _ptr(rows), _ptr(cols), _ptr(ks),
+                                                 _ptr(idx), _ptr(agg), _ptr(G)), "accumulate")
+
+
+def optimizer_step(name: str, G: np.ndarray, x: np.ndarray, m=None, v=None, *, N: int, T: int,
+                   lr: float, momentum: float = 0.0, beta1: float = 0.9, beta2: float = 0.999,
+                   eps: float = 1e-8, weight_decay: float = 0.0) -> None:
+    """x (and the optimiser state m, v) updated in place from G."""
+    _f32c(G, "G"), _f32c(x, "x")
+    for a, nm in ((m, "m"), (v, "v")):
+        if a is not None:
+            _f32c(a, nm)
+    _check(_load().oracle_optimizer(OPTIMIZERS[name], N, x.shape[0], T, lr, momentum, beta1,
+                                    beta2, eps, weight_decay, _ptr(G), _ptr(x), _ptr(m),
+                                    _ptr(v)), "optimizer")

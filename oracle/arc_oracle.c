@@ -451,3 +451,127 @@ done:
   if (!sigma_out) free(sigma);
   return rc;
 }
+
+/* ---------------------------------------------------------------------------
+ * The model step around the compressor: Eq. (11c), the optimisers of the
+ * experiments (Sec. VI) and the dense warm-up before compression starts.
+ *
+ * The nodes never see each other's g^(i); what the second All-Reduce of
+ * Alg. 1 delivers each step is the summed payload.  So every node keeps
+ * G_t = sum_i g_t^(i) by adding that payload, G_t = G_{t-1} + agg_t on the
+ * selected coordinates, and Eq. (11c) reads x_{t+1} = x_t - (gamma/N) G_t.
+ * In exact arithmetic this equals the sum over the nodes' trackers.
+ * ------------------------------------------------------------------------- */
+
+/* Dense (identity-compressor) step: Eq. (11a), then Eq. (11b) with C = I,
+ * the payload added straight into G.  Per coordinate e:
+ *   Delta_i = h_i - g_i, acc = Delta_0 + Delta_1 + ... (ascending i),
+ *   g_i = fl(g_i + Delta_i), G[e] = fl(G[e] + acc).                       */
+int oracle_dense_step(int32_t N, int64_t d, float eta, const void *grad,
+                      int32_t grad_is_bf16, float *h, float *g, float *G) {
+  if (N < 1 || d < 1 || grad == NULL || h == NULL || g == NULL || G == NULL) return 1;
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) return 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < d; ++e) {
+    float acc = 0.0f;
+    for (int32_t i = 0; i < N; ++i) {
+      const int64_t at = (int64_t)i * d + e;
+      const float delta = h[at] - g[at];
+      acc = (i == 0) ? delta : acc + delta;
+      g[at] = g[at] + delta;
+    }
+    G[e] = G[e] + acc;
+  }
+  return 0;
+}
+
+/* G += agg at the selected rows of one m x n view: agg row q goes to the
+ * coordinates [idx[q]*n, idx[q]*n + n) clipped at d. */
+int oracle_accumulate_rows(int64_t d, int64_t n, int64_t K_total,
+                           const int32_t *idx, const float *agg, float *G) {
+  if (d < 1 || n < 1 || K_total < 0 || G == NULL) return 1;
+  if (K_total > 0 && (idx == NULL || agg == NULL)) return 1;
+  const int64_t m = ceil_div(d, n);
+  for (int64_t q = 0; q < K_total; ++q)
+    if (idx[q] < 0 || idx[q] >= m) return 1;
+  for (int64_t q = 0; q < K_total; ++q)
+    for (int64_t j = 0; j < n; ++j) {
+      const int64_t e = (int64_t)idx[q] * n + j;
+      if (e < d) G[e] = G[e] + agg[q * n + j];
+    }
+  return 0;
+}
+
+/* The same for the per-tensor layout: tensor b's selected rows (global row
+ * numbers, tensors' rows in order) carry cols[b] values each in the packed
+ * payload. */
+int oracle_accumulate_tensors(int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K,
+                              const int32_t *idx, const float *agg, float *G) {
+  if (num_tensors < 1 || rows == NULL || cols == NULL || K == NULL || G == NULL) return 1;
+  int64_t off = 0, row0 = 0, q0 = 0, a0 = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) {
+    const int64_t kb = K[b] < rows[b] ? (K[b] < 0 ? 0 : K[b]) : rows[b];
+    for (int64_t q = 0; q < kb; ++q) {
+      const int64_t p = (int64_t)idx[q0 + q] - row0;
+      if (p < 0 || p >= rows[b]) return 1;
+      for (int64_t j = 0; j < cols[b]; ++j) {
+        const int64_t e = off + p * cols[b] + j;
+        G[e] = G[e] + agg[a0 + q * cols[b] + j];
+      }
+    }
+    off += rows[b] * cols[b];
+    row0 += rows[b];
+    q0 += kb;
+    a0 += kb * cols[b];
+  }
+  return 0;
+}
+
+/* Model update x_{t+1} from G_t, coordinate by coordinate.  The direction is
+ * the node average plus the L2 term: dir = fmaf(wd, x, G / N).
+ *   SGD  (Eq. (11c)):  x = fmaf(-lr, dir, x)
+ *   MSGD (heavy ball): u = fmaf(beta, u, dir);  x = fmaf(-lr, u, x)
+ *   Adam (Kingma & Ba, Alg. 1 of "Adam", step count T >= 1):
+ *     m = fmaf(beta1, m, fl((1 - beta1) * dir))
+ *     v = fmaf(beta2, v, fl((1 - beta2) * fl(dir * dir)))
+ *     x = fmaf(-lr, fl(fl(m / c1) / fl(sqrt(fl(v / c2)) + eps)), x)
+ *   with c1 = fl(1 - beta1^T), c2 = fl(1 - beta2^T): beta^T as T binary64
+ *   multiplications of 1.0 by beta, 1 - beta^T in binary64, rounded once to
+ *   binary32; (1 - beta) is rounded to binary32.
+ * optimizer: 0 SGD, 1 MSGD (state m = u), 2 Adam (state m, v). */
+int oracle_optimizer(int32_t optimizer, int32_t N, int64_t d, int64_t T,
+                     float lr, float momentum, float beta1, float beta2,
+                     float eps, float weight_decay, const float *G, float *x,
+                     float *m, float *v) {
+  if (N < 1 || d < 1 || G == NULL || x == NULL) return 1;
+  if (optimizer < 0 || optimizer > 2) return 1;
+  if (optimizer >= 1 && m == NULL) return 1;
+  if (optimizer == 2 && (v == NULL || T < 1)) return 1;
+  const float fN = (float)N;
+  const float b1c = 1.0f - beta1, b2c = 1.0f - beta2;
+  double p1 = 1.0, p2 = 1.0;
+  if (optimizer == 2)
+    for (int64_t s = 0; s < T; ++s) {
+      p1 *= (double)beta1;
+      p2 *= (double)beta2;
+    }
+  const float c1 = (float)(1.0 - p1), c2 = (float)(1.0 - p2);
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < d; ++e) {
+    const float dir = fmaf(weight_decay, x[e], G[e] / fN);
+    if (optimizer == 0) {
+      x[e] = fmaf(-lr, dir, x[e]);
+    } else if (optimizer == 1) {
+      m[e] = fmaf(momentum, m[e], dir);
+      x[e] = fmaf(-lr, m[e], x[e]);
+    } else {
+      m[e] = fmaf(beta1, m[e], b1c * dir);
+      v[e] = fmaf(beta2, v[e], b2c * (dir * dir));
+      const float mh = m[e] / c1, vh = v[e] / c2;
+      const float step = mh / (sqrtf(vh) + eps);
+      x[e] = fmaf(-lr, step, x[e]);
+    }
+  }
+  return 0;
+}

@@ -97,6 +97,27 @@ int oracle_step_tensors(int32_t N, int32_t r, float eta, uint64_t seed,
                         float *g, int32_t *idx, float *agg, int64_t *K_total,
                         int64_t *agg_len, float *sigma_out, float *S_out);
 
+/* Model step around the compressor (Eq. (11c), Sec. VI optimisers and dense
+ * warm-up).  G is the node-summed tracker sum_i g^(i), kept by adding each
+ * step's payload.  Dense step: Eq. (11a) and (11b) with the identity
+ * compressor, the payload added straight into G. */
+int oracle_dense_step(int32_t N, int64_t d, float eta, const void *grad,
+                      int32_t grad_is_bf16, float *h, float *g, float *G);
+
+/* G += agg at the selected rows (single m x n view, or per-tensor packed). */
+int oracle_accumulate_rows(int64_t d, int64_t n, int64_t K_total,
+                           const int32_t *idx, const float *agg, float *G);
+int oracle_accumulate_tensors(int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K,
+                              const int32_t *idx, const float *agg, float *G);
+
+/* x update from G: optimizer 0 SGD (Eq. (11c)), 1 MSGD, 2 Adam; T is Adam's
+ * step count (>= 1); m, v are the optimiser state ([d] each, as needed). */
+int oracle_optimizer(int32_t optimizer, int32_t N, int64_t d, int64_t T,
+                     float lr, float momentum, float beta1, float beta2,
+                     float eps, float weight_decay, const float *G, float *x,
+                     float *m, float *v);
+
 /* Number of threads the oracle's parallel loops use. */
 int oracle_num_threads(void);
 
