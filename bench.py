@@ -142,6 +142,32 @@ def cpu_baseline(w, grads_dev, seconds_target=12.0):
     }
 
 
+def model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb, t0, steps=5, warmup=2):
+    """The full EF21M iteration (11a)-(11c): the compressor step, the payload
+    added into G, and an Adam update of x over all d coordinates
+    (arc_model_step), timed on the library's stream after the main timed
+    region.  Reported beside the compressor-only value."""
+    dev = h.device
+    G, x, m, v = (torch.zeros(w.d, dtype=torch.float32, device=dev) for _ in range(4))
+    mc = arc.make_model_config("adam", lr=1e-3, weight_decay=5e-4)
+    for k in range(warmup):
+        comp.model_step(t0 + k, grads[(t0 + k) % nb], h, g, G, x, mc, m, v)
+    stream.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(steps):
+        t = t0 + warmup + k
+        comp.model_step(t, grads[t % nb], h, g, G, x, mc, m, v)
+    end.record(stream)
+    end.synchronize()
+    ms = start.elapsed_time(end) / steps
+    del G, x, m, v
+    opt_bytes = 28 * w.d  # Adam: read G, x, m, v; write x, m, v
+    return {"optimizer": "adam", "ms_per_iteration": ms, "steps": steps,
+            "gradient_elements_per_s": w.N * w.d / (ms * 1e-3),
+            "adam_update_bytes": opt_bytes}
+
+
 def copy_calibration(torch, gib, reps):
     """Plain device-to-device copy of a known size: every launch reads and
     writes `gib` GiB exactly once."""
@@ -171,6 +197,8 @@ def main():
     ap.add_argument("--batches", type=int, default=4,
                     help="distinct gradient batches kept resident and cycled")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-model-step", action="store_true",
+                    help="skip the extra timing of the full EF21M iteration with Adam")
     ap.add_argument("--print-kernel-digest", action="store_true",
                     help="print the digest of the sketch kernel source and exit")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
@@ -235,6 +263,10 @@ def main():
         total_ms = start.elapsed_time(end)
         stage_ms, nsteps = arc.arc_timing_read(comp.ctx)
         arc.arc_timing_enable(comp.ctx, False)
+        model = None
+        if not args.no_model_step:
+            model = model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb,
+                                      args.warmup + args.steps)
     ms_per_step = total_ms / args.steps
     stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
     log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
@@ -291,6 +323,7 @@ def main():
             "mean_launch_ms": sk_ms,
         },
         "cpu_baseline": cpu,
+        "ef21m_iteration": model,
     }
     print(json.dumps(out), flush=True)
 

@@ -157,6 +157,56 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
 arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
                     float *g, int32_t *out_idx, float *out_agg);
 
+/*
+ * The model step around the compressor (Eq. (11c), the optimisers of the
+ * experiments in Sec. VI, and the dense iterations before compression
+ * starts).  The nodes keep G = sum_i g^(i): each step's summed payload is
+ * added to G at the coordinates it covers, and Eq. (11c) becomes
+ * x <- x - (lr / N) * G for SGD.
+ *
+ * For every coordinate, with dir = fmaf(weight_decay, x, G / N):
+ *   ARC_OPT_SGD:  x = fmaf(-lr, dir, x)
+ *   ARC_OPT_MSGD: m = fmaf(momentum, m, dir);  x = fmaf(-lr, m, x)
+ *   ARC_OPT_ADAM: m = fmaf(beta1, m, fl((1-beta1) * dir));
+ *                 v = fmaf(beta2, v, fl((1-beta2) * fl(dir * dir)));
+ *                 x = fmaf(-lr, fl(fl(m / c1) / fl(sqrt(fl(v / c2)) + eps)), x)
+ *   with T = t + 1, c1 = fl(1 - beta1^T), c2 = fl(1 - beta2^T) (beta^T as T
+ *   binary64 products, 1 - beta^T in binary64, rounded once) and (1 - beta)
+ *   rounded to binary32.  All operations binary32, correctly rounded.
+ */
+typedef enum { ARC_OPT_SGD = 0, ARC_OPT_MSGD = 1, ARC_OPT_ADAM = 2 } arc_optimizer;
+
+typedef struct {
+  int32_t optimizer;   /* arc_optimizer                                      */
+  int32_t dense_steps; /* iterations t < dense_steps are dense (see below)   */
+  float lr;            /* step size gamma, finite                            */
+  float momentum;      /* MSGD, in [0, 1)                                    */
+  float beta1, beta2;  /* Adam, in [0, 1)                                    */
+  float eps;           /* Adam, >= 0                                         */
+  float weight_decay;  /* L2 coefficient, finite                             */
+} arc_model_config;
+
+/*
+ * One EF21M iteration (11a)-(11c) on the context's stream.
+ *   t < dense_steps: the identity compressor (no compression yet): for every
+ *     coordinate, Eq. (11a), Delta_i = h_i - g_i, g_i = g_i + Delta_i, and
+ *     G = G + (Delta_0 + Delta_1 + ...); out_idx and out_agg are not written.
+ *     The same bits as arc_step with every row kept followed by G += agg.
+ *   otherwise: arc_step (same outputs), and G = G + agg at the selected
+ *     coordinates.
+ * Then the optimiser updates x (and opt_m, opt_v) over all d coordinates.
+ *   G, x          device [d] binary32, in/out; G starts at sum_i g^(i) (0 for
+ *                 h = g = 0)
+ *   opt_m, opt_v  device [d] binary32 optimiser state: opt_m for MSGD and
+ *                 Adam, opt_v for Adam (start at 0); may be NULL otherwise
+ * G, x, opt_m and opt_v must not overlap one another or grad, h, g.
+ * 16-byte aligned pointers with d % 4 == 0 take the vectorised kernels.
+ * Invalid model settings give ARC_ERR_INVALID before any work is enqueued.
+ */
+arc_status arc_model_step(arc_ctx *ctx, const arc_model_config *mc, int64_t t,
+                          const void *grad, float *h, float *g, float *G, float *x,
+                          float *opt_m, float *opt_v, int32_t *out_idx, float *out_agg);
+
 /* Release the context and its workspace.  NULL is accepted.  Waits for the
  * context's stream to finish its work first. */
 arc_status arc_destroy(arc_ctx *ctx);

@@ -9,11 +9,12 @@ from __future__ import annotations
 
 from ._lib import (  # noqa: F401
     ARC_DTYPE_BF16, ARC_DTYPE_F32, ARC_ERR_DEVICE, ARC_ERR_INVALID, ARC_ERR_NOMEM,
-    ARC_ERR_UNSUPPORTED, ARC_MAX_R, ARC_NUM_STAGES, ARC_OK, EXPORTED, LIB_PATH, STAGE_NAMES,
-    ArcError, arc_config, arc_create, arc_debug_projection, arc_describe, arc_debug_sigma, arc_debug_sketch,
-    arc_destroy, arc_last_error, arc_num_rows, arc_payload_elems, arc_projection,
-    arc_selected_rows, arc_set_projection, arc_status_str, arc_step, arc_tensor,
-    arc_timing_enable, arc_timing_read, make_config)
+    ARC_ERR_UNSUPPORTED, ARC_MAX_R, ARC_NUM_STAGES, ARC_OK, ARC_OPT_ADAM, ARC_OPT_MSGD,
+    ARC_OPT_SGD, EXPORTED, LIB_PATH, OPTIMIZERS, STAGE_NAMES, ArcError, arc_config, arc_create,
+    arc_debug_projection, arc_describe, arc_debug_sigma, arc_debug_sketch, arc_destroy,
+    arc_last_error, arc_model_config, arc_model_step, arc_num_rows, arc_payload_elems,
+    arc_projection, arc_selected_rows, arc_set_projection, arc_status_str, arc_step, arc_tensor,
+    arc_timing_enable, arc_timing_read, make_config, make_model_config)
 
 
 class Compressor:
@@ -46,6 +47,16 @@ class Compressor:
 
     def step(self, t, grad, h, g):
         arc_step(self.ctx, t, grad, h, g, self.idx, self.agg)
+        agg = self.agg[: self.payload]
+        if self.tensors is None:
+            agg = agg.view(self.K_total, self.n)
+        return self.idx[: self.K_total], agg
+
+    def model_step(self, t, grad, h, g, G, x, mc, opt_m=None, opt_v=None):
+        """One EF21M iteration with the model update (arc_model_step); mc is an
+        arc_model_config (see make_model_config).  Returns (idx, agg) as step()
+        does; on dense iterations they are not written."""
+        arc_model_step(self.ctx, mc, t, grad, h, g, G, x, opt_m, opt_v, self.idx, self.agg)
         agg = self.agg[: self.payload]
         if self.tensors is None:
             agg = agg.view(self.K_total, self.n)

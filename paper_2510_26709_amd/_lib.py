@@ -64,11 +64,36 @@ class arc_config(ctypes.Structure):
     ]
 
 
+ARC_OPT_SGD, ARC_OPT_MSGD, ARC_OPT_ADAM = 0, 1, 2
+OPTIMIZERS = {"sgd": ARC_OPT_SGD, "msgd": ARC_OPT_MSGD, "adam": ARC_OPT_ADAM}
+
+
+class arc_model_config(ctypes.Structure):
+    _fields_ = [
+        ("optimizer", ctypes.c_int32),
+        ("dense_steps", ctypes.c_int32),
+        ("lr", ctypes.c_float),
+        ("momentum", ctypes.c_float),
+        ("beta1", ctypes.c_float),
+        ("beta2", ctypes.c_float),
+        ("eps", ctypes.c_float),
+        ("weight_decay", ctypes.c_float),
+    ]
+
+
+def make_model_config(optimizer="sgd", *, lr, dense_steps=0, momentum=0.0, beta1=0.9,
+                      beta2=0.999, eps=1e-8, weight_decay=0.0) -> arc_model_config:
+    kind = OPTIMIZERS[optimizer] if isinstance(optimizer, str) else int(optimizer)
+    return arc_model_config(kind, dense_steps, lr, momentum, beta1, beta2, eps, weight_decay)
+
+
 _st = ctypes.c_int
 _vp = ctypes.c_void_p
 _SIGS = {
     "arc_create": (_st, [ctypes.POINTER(arc_config), _vp, ctypes.POINTER(_vp)]),
     "arc_step": (_st, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp]),
+    "arc_model_step": (_st, [_vp, ctypes.POINTER(arc_model_config), ctypes.c_int64, _vp, _vp,
+                             _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "arc_destroy": (_st, [_vp]),
     "arc_num_rows": (ctypes.c_int64, [_vp]),
     "arc_selected_rows": (ctypes.c_int64, [_vp]),
@@ -159,6 +184,13 @@ def arc_create(cfg: arc_config, hip_stream=None) -> int:
 def arc_step(ctx: int, t: int, grad, h, g, out_idx, out_agg) -> None:
     _check(_lib.arc_step(ctx, t, _addr(grad), _addr(h), _addr(g), _addr(out_idx),
                          _addr(out_agg)), "arc_step")
+
+
+def arc_model_step(ctx: int, mc: arc_model_config, t: int, grad, h, g, G, x, opt_m, opt_v,
+                   out_idx, out_agg) -> None:
+    _check(_lib.arc_model_step(ctx, ctypes.byref(mc), t, _addr(grad), _addr(h), _addr(g),
+                               _addr(G), _addr(x), _addr(opt_m), _addr(opt_v), _addr(out_idx),
+                               _addr(out_agg)), "arc_model_step")
 
 
 def arc_destroy(ctx) -> None:

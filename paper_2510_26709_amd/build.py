@@ -8,10 +8,11 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libarctopk.so")
 
 # Strict binary32 semantics (no contraction beyond explicit fmaf, no fast-math,
-# denormals kept) and no packed-FP32 instructions.
+# denormals kept, correctly rounded division and square root) and no
+# packed-FP32 instructions.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
-             "-ffp-contract=off", "-fno-fast-math", "-Wall",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+             "-ffp-contract=off", "-fno-fast-math", "-fhip-fp32-correctly-rounded-divide-sqrt",
+             "-Wall", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 def sources():

@@ -558,13 +558,19 @@ int64_t arc_selected_rows(const arc_ctx* ctx) { return ctx ? ctx->K_total : -1; 
 
 int64_t arc_payload_elems(const arc_ctx* ctx) { return ctx ? ctx->payload : -1; }
 
-arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
-                    int32_t* out_idx, float* out_agg) {
+}  // extern "C"
+
+namespace {
+
+// need_outputs: the call writes out_idx / out_agg (every compressed step).
+arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const float* h,
+                           const float* g, const int32_t* out_idx, const float* out_agg,
+                           bool need_outputs) {
   if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
   if (t < 0) return fail(ARC_ERR_INVALID, "t must be >= 0");
   if (grad == nullptr || h == nullptr || g == nullptr)
     return fail(ARC_ERR_INVALID, "grad, h and g must be non-NULL");
-  if (c->K_total > 0 && (out_idx == nullptr || out_agg == nullptr))
+  if (need_outputs && c->K_total > 0 && (out_idx == nullptr || out_agg == nullptr))
     return fail(ARC_ERR_INVALID, "out_idx and out_agg must be non-NULL");
   const size_t elems = static_cast<size_t>(c->N) * static_cast<size_t>(c->d);
   const size_t grad_bytes = elems * (c->grad_bf16 ? 2 : 4), state_bytes = elems * 4;
@@ -572,7 +578,13 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
       ranges_overlap(grad, grad_bytes, g, state_bytes) ||
       ranges_overlap(h, state_bytes, g, state_bytes))
     return fail(ARC_ERR_INVALID, "grad, h and g must not overlap");
+  return ARC_OK;
+}
 
+// The compressor step (arguments already checked); with a non-null G the
+// payload is also added into G at the selected coordinates.
+arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                        int32_t* out_idx, float* out_agg, float* G) {
   // Vectorisable groups take the 16-byte kernels only when the three streams
   // are 16-byte aligned; otherwise every group takes the general kernel.
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
@@ -626,20 +638,111 @@ arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
   ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
   if ((st = record(c, slot, 4))) return st;
   // Stage 3: gather + worker sum + error-feedback update.
+  const bool G_ok = G == nullptr || aligned16(G);
   if (c->tensor_mode) {
-    const bool vec_ok = aligned16(h) && aligned16(g) && aligned16(out_agg);
-    ARC_HIP(arc::launch_gather_update_tensors(h, g, out_idx, out_agg, c->gather_dev,
+    const bool vec_ok = aligned16(h) && aligned16(g) && aligned16(out_agg) && G_ok;
+    ARC_HIP(arc::launch_gather_update_tensors(h, g, out_idx, out_agg, G, c->gather_dev,
                                               static_cast<int32_t>(c->gather.size()),
                                               c->gather_work, c->d, c->N, vec_ok, c->stream),
             "gather launch");
   } else {
     const bool fast_gather = c->n % 4 == 0 && c->d % 4 == 0 && aligned16(h) && aligned16(g) &&
-                             aligned16(out_agg);
-    ARC_HIP(arc::launch_gather_update(fast_gather, h, g, out_idx, out_agg, c->K_total, c->d,
+                             aligned16(out_agg) && G_ok;
+    ARC_HIP(arc::launch_gather_update(fast_gather, h, g, out_idx, out_agg, G, c->K_total, c->d,
                                       c->n, c->m, c->N, c->stream),
             "gather launch");
   }
   if ((st = record(c, slot, 5))) return st;
+  return ARC_OK;
+}
+
+bool finite(float v) { return std::isfinite(v); }
+
+}  // namespace
+
+extern "C" {
+
+arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                    int32_t* out_idx, float* out_agg) {
+  const arc_status st = check_step_args(c, t, grad, h, g, out_idx, out_agg, true);
+  if (st != ARC_OK) return st;
+  return enqueue_step(c, t, grad, h, g, out_idx, out_agg, nullptr);
+}
+
+arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, const void* grad,
+                          float* h, float* g, float* G, float* x, float* opt_m, float* opt_v,
+                          int32_t* out_idx, float* out_agg) {
+  if (mc == nullptr) return fail(ARC_ERR_INVALID, "model config is NULL");
+  // A dense iteration writes no payload, so out_idx / out_agg may be NULL.
+  const bool dense = t < mc->dense_steps;
+  arc_status st = check_step_args(c, t, grad, h, g, out_idx, out_agg, !dense);
+  if (st != ARC_OK) return st;
+  if (mc->optimizer < ARC_OPT_SGD || mc->optimizer > ARC_OPT_ADAM)
+    return fail(ARC_ERR_INVALID, "optimizer must be ARC_OPT_SGD, ARC_OPT_MSGD or ARC_OPT_ADAM");
+  if (mc->dense_steps < 0) return fail(ARC_ERR_INVALID, "dense_steps must be >= 0");
+  if (!finite(mc->lr) || !finite(mc->weight_decay))
+    return fail(ARC_ERR_INVALID, "lr and weight_decay must be finite");
+  if (!(mc->momentum >= 0.0f && mc->momentum < 1.0f) ||
+      !(mc->beta1 >= 0.0f && mc->beta1 < 1.0f) || !(mc->beta2 >= 0.0f && mc->beta2 < 1.0f) ||
+      !(mc->eps >= 0.0f) || !finite(mc->eps))
+    return fail(ARC_ERR_INVALID, "momentum, beta1, beta2 must be in [0, 1), eps >= 0");
+  if (G == nullptr || x == nullptr) return fail(ARC_ERR_INVALID, "G and x must be non-NULL");
+  if (mc->optimizer >= ARC_OPT_MSGD && opt_m == nullptr)
+    return fail(ARC_ERR_INVALID, "opt_m must be non-NULL for MSGD and Adam");
+  if (mc->optimizer == ARC_OPT_ADAM && opt_v == nullptr)
+    return fail(ARC_ERR_INVALID, "opt_v must be non-NULL for Adam");
+  {
+    const size_t elems = static_cast<size_t>(c->N) * static_cast<size_t>(c->d);
+    const size_t vb = static_cast<size_t>(c->d) * 4;
+    const void* big[3] = {grad, h, g};
+    const size_t big_bytes[3] = {elems * (c->grad_bf16 ? 2 : 4), elems * 4, elems * 4};
+    const void* vecs[4] = {G, x, mc->optimizer >= ARC_OPT_MSGD ? opt_m : nullptr,
+                           mc->optimizer == ARC_OPT_ADAM ? opt_v : nullptr};
+    for (int a = 0; a < 4; ++a) {
+      if (vecs[a] == nullptr) continue;
+      for (int b = a + 1; b < 4; ++b)
+        if (vecs[b] != nullptr && ranges_overlap(vecs[a], vb, vecs[b], vb))
+          return fail(ARC_ERR_INVALID, "G, x, opt_m and opt_v must not overlap");
+      for (int b = 0; b < 3; ++b)
+        if (ranges_overlap(vecs[a], vb, big[b], big_bytes[b]))
+          return fail(ARC_ERR_INVALID, "G, x, opt_m, opt_v must not overlap grad, h or g");
+    }
+  }
+
+  if (dense) {
+    const bool vec = c->d % 4 == 0 && aligned16(grad) && aligned16(h) && aligned16(g) &&
+                     aligned16(G);
+    ARC_HIP(arc::launch_dense_step(vec, grad, c->grad_bf16, h, g, G, c->d, c->N, c->eta, c->a,
+                                   c->stream),
+            "dense step launch");
+  } else {
+    st = enqueue_step(c, t, grad, h, g, out_idx, out_agg, G);
+    if (st != ARC_OK) return st;
+  }
+
+  arc::OptimizerArgs o{};
+  o.kind = mc->optimizer;
+  o.neg_lr = -mc->lr;
+  o.momentum = mc->momentum;
+  o.beta1 = mc->beta1;
+  o.beta2 = mc->beta2;
+  o.one_minus_beta1 = 1.0f - mc->beta1;
+  o.one_minus_beta2 = 1.0f - mc->beta2;
+  double p1 = 1.0, p2 = 1.0;
+  if (mc->optimizer == ARC_OPT_ADAM)
+    for (int64_t k = 0; k <= t; ++k) {  // beta^T with T = t + 1
+      p1 *= static_cast<double>(mc->beta1);
+      p2 *= static_cast<double>(mc->beta2);
+    }
+  o.c1 = static_cast<float>(1.0 - p1);
+  o.c2 = static_cast<float>(1.0 - p2);
+  o.eps = mc->eps;
+  o.weight_decay = mc->weight_decay;
+  o.fN = static_cast<float>(c->N);
+  const bool vec = c->d % 4 == 0 && aligned16(G) && aligned16(x) &&
+                   (o.kind < 1 || aligned16(opt_m)) && (o.kind < 2 || aligned16(opt_v));
+  ARC_HIP(arc::launch_optimizer(vec, o, G, x, opt_m, opt_v, c->d, c->stream),
+          "optimizer launch");
   return ARC_OK;
 }
 

@@ -135,18 +135,42 @@ hipError_t launch_reduce_importance(const float* S, float* sigma,
 hipError_t launch_select(const float* sigma, const SelectWorkspace& ws,
                          int32_t* out_idx, hipStream_t stream);
 
-// Gather of the selected rows, worker sum into agg, g += Delta on them.
+// Gather of the selected rows, worker sum into agg, g += Delta on them, and
+// G += agg there when G is non-null (fast: G 16-byte aligned as well).
 hipError_t launch_gather_update(bool fast, const float* h, float* g,
-                                const int32_t* idx, float* agg, int64_t K_total,
+                                const int32_t* idx, float* agg, float* G, int64_t K_total,
                                 int64_t d, int64_t n, int64_t m, int32_t N,
                                 hipStream_t stream);
 
 // Per-tensor mode gather: buckets[0 .. nb), work items total_work.
 hipError_t launch_gather_update_tensors(const float* h, float* g,
-                                        const int32_t* idx, float* agg,
+                                        const int32_t* idx, float* agg, float* G,
                                         const GatherBucket* buckets, int32_t nb,
                                         int64_t total_work, int64_t d, int32_t N,
                                         bool allow_vec, hipStream_t stream);
+
+// Model step (arc_model.hip).  Dense step: Eq. (11a), (11b) with the identity
+// compressor, payload added into G, every coordinate (vec: 16-byte aligned
+// pointers and d % 4 == 0).
+hipError_t launch_dense_step(bool vec, const void* grad, int32_t grad_bf16, float* h,
+                             float* g, float* G, int64_t d, int32_t N, float eta, float a,
+                             hipStream_t stream);
+
+// Optimiser constants of one x update (host-computed).
+struct OptimizerArgs {
+  int32_t kind;        // 0 SGD, 1 MSGD, 2 Adam
+  float neg_lr;        // -lr
+  float momentum;      // MSGD beta
+  float beta1, beta2;  // Adam
+  float one_minus_beta1, one_minus_beta2;  // fl(1 - beta)
+  float c1, c2;        // Adam bias corrections fl(1 - beta^T)
+  float eps, weight_decay;
+  float fN;            // number of nodes
+};
+
+// x (and m, v) updated from G over every coordinate.
+hipError_t launch_optimizer(bool vec, const OptimizerArgs& o, const float* G, float* x,
+                            float* m, float* v, int64_t d, hipStream_t stream);
 
 // ---- host projection (arc_projection.cpp) ----
 // V_t (n x r, row-major) for the shared seed and step t.

@@ -1,5 +1,7 @@
 // Gather + worker sum + error-feedback update of the compressor step (Eq. (5),
-// Alg. 1's payload All-Reduce, Eq. (11b)).
+// Alg. 1's payload All-Reduce, Eq. (11b)).  With a non-null G the summed
+// payload is also added into the node-summed tracker, G = fl(G + agg), at the
+// same coordinates (the model step's view of the payload, Eq. (11c)).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -20,8 +22,8 @@ constexpr int kMaxUnrolledWorkers = 8;
 __global__ void __launch_bounds__(256)
 gather_update_fast_kernel(const float* __restrict__ h, float* __restrict__ g,
                           const int32_t* __restrict__ idx,
-                          float* __restrict__ agg, int64_t K_total, int64_t d,
-                          int64_t n, int64_t m, int32_t N) {
+                          float* __restrict__ agg, float* __restrict__ G, int64_t K_total,
+                          int64_t d, int64_t n, int64_t m, int32_t N) {
   const int64_t per_row = n / 4;
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (tid >= K_total * per_row) return;
@@ -71,6 +73,14 @@ gather_update_fast_kernel(const float* __restrict__ h, float* __restrict__ g,
         }
       }
     }
+    if (G) {
+      float4 Gv = *reinterpret_cast<const float4*>(G + e);
+      Gv.x = Gv.x + acc.x;
+      Gv.y = Gv.y + acc.y;
+      Gv.z = Gv.z + acc.z;
+      Gv.w = Gv.w + acc.w;
+      *reinterpret_cast<float4*>(G + e) = Gv;
+    }
   } else {
     float a4[4] = {0.f, 0.f, 0.f, 0.f};
     for (int jj = 0; jj < 4; ++jj) {
@@ -81,6 +91,7 @@ gather_update_fast_kernel(const float* __restrict__ h, float* __restrict__ g,
         a4[jj] = (i == 0) ? dl : a4[jj] + dl;
         g[at] = g[at] + dl;
       }
+      if (G) G[e + jj] = G[e + jj] + a4[jj];
     }
     acc = make_float4(a4[0], a4[1], a4[2], a4[3]);
   }
@@ -90,7 +101,7 @@ gather_update_fast_kernel(const float* __restrict__ h, float* __restrict__ g,
 __global__ void __launch_bounds__(256)
 gather_update_generic_kernel(const float* __restrict__ h, float* __restrict__ g,
                              const int32_t* __restrict__ idx,
-                             float* __restrict__ agg, int64_t K_total,
+                             float* __restrict__ agg, float* __restrict__ G, int64_t K_total,
                              int64_t d, int64_t n, int64_t m, int32_t N) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (tid >= K_total * n) return;
@@ -106,6 +117,7 @@ gather_update_generic_kernel(const float* __restrict__ h, float* __restrict__ g,
       acc = (i == 0) ? dl : acc + dl;
       g[at] = g[at] + dl;
     }
+    if (G) G[e] = G[e] + acc;
   }
   agg[tid] = acc;
 }
@@ -119,7 +131,7 @@ gather_update_generic_kernel(const float* __restrict__ h, float* __restrict__ g,
 __global__ void __launch_bounds__(256)
 gather_update_tensors_kernel(const float* __restrict__ h, float* __restrict__ g,
                              const int32_t* __restrict__ idx,
-                             float* __restrict__ agg,
+                             float* __restrict__ agg, float* __restrict__ G,
                              const GatherBucket* __restrict__ buckets,
                              int32_t nb, int64_t total_work, int64_t d,
                              int32_t N, int32_t allow_vec) {
@@ -168,6 +180,14 @@ gather_update_tensors_kernel(const float* __restrict__ h, float* __restrict__ g,
       gn.w = gv.w + dl.w;
       *reinterpret_cast<float4*>(g + at) = gn;
     }
+    if (G) {
+      float4 Gv = *reinterpret_cast<const float4*>(G + e);
+      Gv.x = Gv.x + acc.x;
+      Gv.y = Gv.y + acc.y;
+      Gv.z = Gv.z + acc.z;
+      Gv.w = Gv.w + acc.w;
+      *reinterpret_cast<float4*>(G + e) = Gv;
+    }
     *reinterpret_cast<float4*>(out) = acc;
   } else {
     for (int64_t jj = 0; jj < ncols; ++jj) {
@@ -178,6 +198,7 @@ gather_update_tensors_kernel(const float* __restrict__ h, float* __restrict__ g,
         acc = (i == 0) ? dl : acc + dl;
         g[at] = g[at] + dl;
       }
+      if (G) G[e + jj] = G[e + jj] + acc;
       out[jj] = acc;
     }
   }
@@ -186,30 +207,30 @@ gather_update_tensors_kernel(const float* __restrict__ h, float* __restrict__ g,
 }  // namespace
 
 hipError_t launch_gather_update(bool fast, const float* h, float* g,
-                                const int32_t* idx, float* agg, int64_t K_total,
+                                const int32_t* idx, float* agg, float* G, int64_t K_total,
                                 int64_t d, int64_t n, int64_t m, int32_t N,
                                 hipStream_t stream) {
   if (K_total <= 0) return hipSuccess;
   if (fast) {
     hipLaunchKernelGGL(gather_update_fast_kernel,
                        dim3(blocks_for(K_total * (n / 4), 256)), dim3(256), 0,
-                       stream, h, g, idx, agg, K_total, d, n, m, N);
+                       stream, h, g, idx, agg, G, K_total, d, n, m, N);
   } else {
     hipLaunchKernelGGL(gather_update_generic_kernel,
                        dim3(blocks_for(K_total * n, 256)), dim3(256), 0, stream,
-                       h, g, idx, agg, K_total, d, n, m, N);
+                       h, g, idx, agg, G, K_total, d, n, m, N);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gather_update_tensors(const float* h, float* g,
-                                        const int32_t* idx, float* agg,
+                                        const int32_t* idx, float* agg, float* G,
                                         const GatherBucket* buckets, int32_t nb,
                                         int64_t total_work, int64_t d, int32_t N,
                                         bool allow_vec, hipStream_t stream) {
   if (total_work <= 0) return hipSuccess;
   hipLaunchKernelGGL(gather_update_tensors_kernel, dim3(blocks_for(total_work, 256)),
-                     dim3(256), 0, stream, h, g, idx, agg, buckets, nb, total_work, d, N,
+                     dim3(256), 0, stream, h, g, idx, agg, G, buckets, nb, total_work, d, N,
                      allow_vec ? 1 : 0);
   return hipGetLastError();
 }

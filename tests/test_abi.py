@@ -187,3 +187,30 @@ def test_projection_rejects_bad_arguments(args):
     with pytest.raises(arc.ArcError):
         arc.arc_projection(*args, buf)
     assert _lib._lib.arc_projection(1, 0, 4, 4, None) == arc.ARC_ERR_INVALID
+
+
+def test_model_config_layout_matches_header(tmp_path):
+    src = tmp_path / "mlayout.c"
+    fields = [f for f, _ in _lib.arc_model_config._fields_]
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "libarctopk.h"\n'
+        'int main(void){printf("%zu", sizeof(arc_model_config));'
+        + "".join(f'printf(" %zu", offsetof(arc_model_config, {f}));' for f in fields)
+        + "return 0;}\n")
+    exe = tmp_path / "mlayout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    assert vals[0] == ctypes.sizeof(_lib.arc_model_config)
+    for f, off in zip(fields, vals[1:]):
+        assert getattr(_lib.arc_model_config, f).offset == off, f
+
+
+def test_model_step_rejects_null_context_and_config():
+    L = _lib._lib
+    mc = arc.make_model_config("sgd", lr=0.1)
+    assert L.arc_model_step(None, ctypes.byref(mc), 0, 1, 2, 3, 4, 5, None, None, 6, 7) == \
+        arc.ARC_ERR_INVALID
+    assert L.arc_model_step(12345, None, 0, 1, 2, 3, 4, 5, None, None, 6, 7) == \
+        arc.ARC_ERR_INVALID
