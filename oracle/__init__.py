@@ -49,6 +49,16 @@ def _load():
         "oracle_accumulate_tensors": (ctypes.c_int, [_i32, _vp, _vp, _vp, _vp, _vp, _vp]),
         "oracle_optimizer": (ctypes.c_int, [_i32, _i32, _i64, _i64, _f32, _f32, _f32, _f32, _f32,
                                             _f32, _vp, _vp, _vp, _vp]),
+        "oracle_randk_keys": (ctypes.c_int, [_u64, _i64, _i64, _vp]),
+        "oracle_step_randk": (ctypes.c_int, [_i32, _i64, _i64, _f32, _u64, _i64, _i64, _i32, _vp,
+                                             _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "oracle_step_randk_tensors": (ctypes.c_int, [_i32, _f32, _u64, _i64, _i32, _vp, _vp, _vp,
+                                                     _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                                     _vp]),
+        "oracle_step_topk": (ctypes.c_int, [_i32, _i64, _i64, _f32, _i64, _i32, _vp, _vp, _vp,
+                                            _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "oracle_step_topk_tensors": (ctypes.c_int, [_i32, _f32, _i32, _vp, _vp, _vp, _vp, _i32,
+                                                    _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "oracle_num_threads": (ctypes.c_int, []),
     }
     for name, (res, args) in sig.items():
@@ -298,3 +308,110 @@ def optimizer_step(name: str, G: np.ndarray, x: np.ndarray, m=None, v=None, *, N
     _check(_load().oracle_optimizer(OPTIMIZERS[name], N, x.shape[0], T, lr, momentum, beta1,
                                     beta2, eps, weight_decay, _ptr(G), _ptr(x), _ptr(m),
                                     _ptr(v)), "optimizer")
+
+
+# ---- comparison compressors of Table I (Rand-K, Top-K) ----
+
+def randk_keys(seed: int, t: int, m: int) -> np.ndarray:
+    keys = np.empty(m, dtype=np.float32)
+    _check(_load().oracle_randk_keys(seed & (2**64 - 1), t, m, _ptr(keys)), "randk_keys")
+    return keys
+
+
+def _tensor_arrays(tensors):
+    tens = np.asarray(tensors, dtype=np.int64).reshape(-1, 3)
+    return tuple(np.ascontiguousarray(tens[:, c]) for c in range(3))
+
+
+def _kept_rows(m, K, buckets, tensors):
+    if tensors is not None:
+        return int(sum(min(max(int(k), 0), int(r)) for r, _, k in tensors))
+    if buckets is None:
+        return min(m, max(K, 0))
+    begin, kb = buckets
+    return int(sum(min(max(int(k), 0), int(b1 - b0)) for k, b0, b1 in
+                   zip(kb, begin[:-1], begin[1:])))
+
+
+def step_randk(h: np.ndarray, g: np.ndarray, grad: np.ndarray, *, eta: float, seed: int, t: int,
+               n: int = 0, K: int = 0, buckets=None, tensors=None,
+               want_keys: bool = False) -> dict:
+    """Rand-K inside the EF21M step (in place on h, g): {"idx", "agg"} as for
+    step / step_tensors, plus "keys" when asked for."""
+    _f32c(h, "h"), _f32c(g, "g")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    N, d = h.shape
+    if g.shape != h.shape or grad.shape != h.shape:
+        raise ValueError("h, g and grad must all be [N, d]")
+    total, alen = ctypes.c_int64(0), ctypes.c_int64(0)
+    if tensors is None:
+        m = num_rows(d, n)
+        kmax = _kept_rows(m, K, buckets, None)
+        idx = np.empty(max(m, 1), dtype=np.int32)
+        agg = np.empty((max(kmax, 1), n), dtype=np.float32)
+        keys = np.empty(m, dtype=np.float32)
+        nb, begin, kb = _bucket_arrays(buckets)
+        _check(_load().oracle_step_randk(N, d, n, eta, seed & (2**64 - 1), t, K, nb, _ptr(begin),
+                                         _ptr(kb), _ptr(grad), is_bf16, _ptr(h), _ptr(g),
+                                         _ptr(idx), _ptr(agg), ctypes.addressof(total),
+                                         _ptr(keys)), "step_randk")
+        out = {"idx": idx[: total.value].copy(), "agg": agg[: total.value].copy()}
+    else:
+        rows, cols, ks = _tensor_arrays(tensors)
+        m = int(rows.sum())
+        kmax = _kept_rows(m, 0, None, tensors)
+        idx = np.empty(max(m, 1), dtype=np.int32)
+        agg = np.empty(max(int(sum(min(max(int(k), 0), int(r)) * int(c)
+                                   for r, c, k in tensors)), 1), dtype=np.float32)
+        keys = np.empty(m, dtype=np.float32)
+        _check(_load().oracle_step_randk_tensors(N, eta, seed & (2**64 - 1), t, len(rows),
+                                                 _ptr(rows), _ptr(cols), _ptr(ks), _ptr(grad),
+                                                 is_bf16, _ptr(h), _ptr(g), _ptr(idx), _ptr(agg),
+                                                 ctypes.addressof(total), ctypes.addressof(alen),
+                                                 _ptr(keys)), "step_randk_tensors")
+        out = {"idx": idx[: total.value].copy(), "agg": agg[: alen.value].copy()}
+    if want_keys:
+        out["keys"] = keys
+    return out
+
+
+def step_topk(h: np.ndarray, g: np.ndarray, grad: np.ndarray, *, eta: float, n: int = 0,
+              K: int = 0, buckets=None, tensors=None, want_norms: bool = False) -> dict:
+    """Local Top-K inside the EF21M step (in place on h, g): {"idx": int32
+    [N, K_total] (each node's rows), "agg": float32 [N, L] (each node's own
+    rows of Delta, nothing summed)}, plus "norms" [N, m] when asked for."""
+    _f32c(h, "h"), _f32c(g, "g")
+    grad, is_bf16 = _grad_args(np.ascontiguousarray(grad))
+    N, d = h.shape
+    if g.shape != h.shape or grad.shape != h.shape:
+        raise ValueError("h, g and grad must all be [N, d]")
+    total, alen = ctypes.c_int64(0), ctypes.c_int64(0)
+    if tensors is None:
+        m = num_rows(d, n)
+        kmax = _kept_rows(m, K, buckets, None)
+        idx = np.empty(max(N * m, 1), dtype=np.int32)
+        agg = np.empty(max(N * kmax * n, 1), dtype=np.float32)
+        norms = np.empty((N, m), dtype=np.float32)
+        nb, begin, kb = _bucket_arrays(buckets)
+        _check(_load().oracle_step_topk(N, d, n, eta, K, nb, _ptr(begin), _ptr(kb), _ptr(grad),
+                                        is_bf16, _ptr(h), _ptr(g), _ptr(idx), _ptr(agg),
+                                        ctypes.addressof(total), _ptr(norms)), "step_topk")
+        L = total.value * n
+    else:
+        rows, cols, ks = _tensor_arrays(tensors)
+        m = int(rows.sum())
+        Lmax = int(sum(min(max(int(k), 0), int(r)) * int(c) for r, c, k in tensors))
+        idx = np.empty(max(N * m, 1), dtype=np.int32)
+        agg = np.empty(max(N * Lmax, 1), dtype=np.float32)
+        norms = np.empty((N, m), dtype=np.float32)
+        _check(_load().oracle_step_topk_tensors(N, eta, len(rows), _ptr(rows), _ptr(cols),
+                                                _ptr(ks), _ptr(grad), is_bf16, _ptr(h), _ptr(g),
+                                                _ptr(idx), _ptr(agg), ctypes.addressof(total),
+                                                ctypes.addressof(alen), _ptr(norms)),
+               "step_topk_tensors")
+        L = alen.value
+    kt = total.value
+    out = {"idx": idx[: N * kt].reshape(N, kt).copy(), "agg": agg[: N * L].reshape(N, L).copy()}
+    if want_norms:
+        out["norms"] = norms
+    return out

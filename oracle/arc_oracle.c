@@ -341,6 +341,40 @@ done:
   return rc;
 }
 
+/* Gather + worker sum + EF update of the per-tensor layout (Eq. (5), (11b)),
+ * tensor by tensor; tensor b's K_b selected rows (global row numbers) carry
+ * cols[b] values each in the packed payload.  Returns the payload length. */
+static int64_t gather_update_tensors(int32_t N, int64_t d, int32_t num_tensors,
+                                     const int64_t *rows, const int64_t *cols,
+                                     const int64_t *K, const int32_t *idx,
+                                     const float *h, float *g, float *agg) {
+  int64_t off = 0, row0 = 0, q0 = 0, a0 = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) {
+    const int64_t mb = rows[b], nb = cols[b];
+    const int64_t kb = K[b] < mb ? K[b] : mb;
+#pragma omp parallel for schedule(static)
+    for (int64_t q = 0; q < kb; ++q) {
+      const int64_t p = idx[q0 + q] - row0;
+      for (int64_t j = 0; j < nb; ++j) {
+        const int64_t e = off + p * nb + j;
+        float acc = 0.0f;
+        for (int32_t i = 0; i < N; ++i) {
+          const int64_t at = (int64_t)i * d + e;
+          const float delta = h[at] - g[at];
+          acc = (i == 0) ? delta : acc + delta;
+          g[at] = g[at] + delta;
+        }
+        agg[a0 + q * nb + j] = acc;
+      }
+    }
+    off += mb * nb;
+    row0 += mb;
+    q0 += kb;
+    a0 += kb * nb;
+  }
+  return a0;
+}
+
 /* ---------------------------------------------------------------------------
  * Per-tensor mode (Sec. VI): the model's tensors are compressed one by one,
  * each in its own m_b x n_b view (2-D weights as they are, convolution
@@ -416,34 +450,7 @@ int oracle_step_tensors(int32_t N, int32_t r, float eta, uint64_t seed,
     if (bad) goto done;
   }
 
-  /* Gather + worker sum + EF update, tensor by tensor, packed payload. */
-  {
-    int64_t off = 0, row0 = 0, q0 = 0, a0 = 0;
-    for (int32_t b = 0; b < num_tensors; ++b) {
-      const int64_t mb = rows[b], nb = cols[b];
-      const int64_t kb = K[b] < mb ? K[b] : mb;
-#pragma omp parallel for schedule(static)
-      for (int64_t q = 0; q < kb; ++q) {
-        const int64_t p = idx[q0 + q] - row0;
-        for (int64_t j = 0; j < nb; ++j) {
-          const int64_t e = off + p * nb + j;
-          float acc = 0.0f;
-          for (int32_t i = 0; i < N; ++i) {
-            const int64_t at = (int64_t)i * d + e;
-            const float delta = h[at] - g[at];
-            acc = (i == 0) ? delta : acc + delta;
-            g[at] = g[at] + delta;
-          }
-          agg[a0 + q * nb + j] = acc;
-        }
-      }
-      off += mb * nb;
-      row0 += mb;
-      q0 += kb;
-      a0 += kb * nb;
-    }
-    *agg_len = a0;
-  }
+  *agg_len = gather_update_tensors(N, d, num_tensors, rows, cols, K, idx, h, g, agg);
   rc = 0;
 done:
   if (!S_out) free(S);
@@ -574,4 +581,236 @@ int oracle_optimizer(int32_t optimizer, int32_t N, int64_t d, int64_t T,
     }
   }
   return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Comparison compressors of Table I, inside the same EF21M recursion
+ * (11a)-(11b) and on the same m x n row views; each keeps K rows (per bucket
+ * or tensor) of Delta^(i) = h_t^(i) - g_{t-1}^(i).
+ *
+ * Rand-K (Sec. I-A; All-Reduce compatible): K rows drawn uniformly at random,
+ * the same rows on every node (shared seed), unscaled so that the compressor
+ * stays contractive with alpha = K/m.  The draw: row p gets the key
+ * u_p = floor(x / 2^40), x = SplitMix64 output number t*m + p of the stream
+ * seeded with the shared seed (the generator of oracle_splitmix64), as a
+ * binary32 integer in [0, 2^24); the K rows with the largest keys are kept,
+ * ties to the lower row, exactly the arg-top-K of Eq. (4) with u in place of
+ * Sigma.  The payload is summed over nodes as for ARC-Top-K.
+ *
+ * Top-K (Sec. III, Prop. 1; All-Gather): each node keeps its own K rows of
+ * largest squared norm ||Delta^(i)_p||^2 (an fmaf chain of squares over the
+ * row's columns in ascending order from +0), ties to the lower row, and sends
+ * them with their indices; nothing is summed on the wire.  idx holds node i's
+ * rows at [i*K_total, (i+1)*K_total), agg its rows at [i*L, (i+1)*L) with L
+ * the payload length of one node.
+ * ------------------------------------------------------------------------- */
+int oracle_randk_keys(uint64_t seed, int64_t t, int64_t m, float *keys) {
+  if (m < 1 || t < 0 || keys == NULL) return 1;
+#pragma omp parallel for schedule(static)
+  for (int64_t p = 0; p < m; ++p)
+    keys[p] = (float)(oracle_splitmix64(seed, (uint64_t)(t * m + p)) >> 40);
+  return 0;
+}
+
+int oracle_step_randk(int32_t N, int64_t d, int64_t n, float eta, uint64_t seed,
+                      int64_t t, int64_t K_global, int32_t num_buckets,
+                      const int64_t *bucket_row_begin, const int64_t *bucket_K,
+                      const void *grad, int32_t grad_is_bf16, float *h, float *g,
+                      int32_t *idx, float *agg, int64_t *K_total, float *keys_out) {
+  if (N < 1 || d < 1 || n < 1 || K_total == NULL) return 1;
+  const int64_t m = ceil_div(d, n);
+  if (m > INT32_MAX) return 1;
+  float *keys = keys_out ? keys_out : (float *)malloc((size_t)m * sizeof(float));
+  int rc = 1;
+  if (keys == NULL) return 1;
+  if (oracle_randk_keys(seed, t, m, keys)) goto done;
+  /* Validate the selection on the keys before touching the state. */
+  if (oracle_select(m, keys, K_global, num_buckets, bucket_row_begin, bucket_K, idx, K_total))
+    goto done;
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) goto done;
+  if (oracle_gather_update(N, d, n, *K_total, idx, h, g, agg)) goto done;
+  rc = 0;
+done:
+  if (!keys_out) free(keys);
+  return rc;
+}
+
+static int tensor_buckets(int32_t num_tensors, const int64_t *rows, const int64_t *cols,
+                          const int64_t *K, int64_t *d_out, int64_t *m_out,
+                          int64_t **begin_out) {
+  if (num_tensors < 1 || rows == NULL || cols == NULL || K == NULL) return 1;
+  int64_t d = 0, m = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) {
+    if (rows[b] < 1 || cols[b] < 1 || K[b] < 0) return 1;
+    d += rows[b] * cols[b];
+    m += rows[b];
+  }
+  if (m > INT32_MAX) return 1;
+  int64_t *begin = (int64_t *)malloc((size_t)(num_tensors + 1) * sizeof(int64_t));
+  if (begin == NULL) return 1;
+  begin[0] = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) begin[b + 1] = begin[b] + rows[b];
+  *d_out = d;
+  *m_out = m;
+  *begin_out = begin;
+  return 0;
+}
+
+int oracle_step_randk_tensors(int32_t N, float eta, uint64_t seed, int64_t t,
+                              int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K, const void *grad,
+                              int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                              float *agg, int64_t *K_total, int64_t *agg_len,
+                              float *keys_out) {
+  int64_t d, m, *begin = NULL;
+  if (N < 1 || idx == NULL || agg == NULL || K_total == NULL || agg_len == NULL) return 1;
+  if (tensor_buckets(num_tensors, rows, cols, K, &d, &m, &begin)) return 1;
+  float *keys = keys_out ? keys_out : (float *)malloc((size_t)m * sizeof(float));
+  int rc = 1;
+  if (keys == NULL) goto done;
+  if (oracle_randk_keys(seed, t, m, keys)) goto done;
+  if (oracle_select(m, keys, 0, num_tensors, begin, K, idx, K_total)) goto done;
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) goto done;
+  *agg_len = gather_update_tensors(N, d, num_tensors, rows, cols, K, idx, h, g, agg);
+  rc = 0;
+done:
+  if (!keys_out) free(keys);
+  free(begin);
+  return rc;
+}
+
+/* Squared norm of row p of node i's Delta: columns [off, off + len) of the
+ * node's vector, fmaf chain in ascending column order from +0. */
+static float row_norm2(const float *h, const float *g, int64_t off, int64_t len) {
+  float acc = 0.0f;
+  for (int64_t j = 0; j < len; ++j) {
+    const float delta = h[off + j] - g[off + j];
+    acc = fmaf(delta, delta, acc);
+  }
+  return acc;
+}
+
+/* Node i's own rows: payload values are Delta^(i) itself (nothing summed),
+ * and g^(i) = fl(g^(i) + Delta^(i)) on those rows (Eq. (11b)). */
+static void gather_own_row(const float *hi, float *gi, int64_t off, int64_t len, int64_t width,
+                           float *out) {
+  for (int64_t j = 0; j < width; ++j) {
+    if (j >= len) {
+      out[j] = 0.0f;
+      continue;
+    }
+    const float delta = hi[off + j] - gi[off + j];
+    out[j] = delta;
+    gi[off + j] = gi[off + j] + delta;
+  }
+}
+
+int oracle_step_topk(int32_t N, int64_t d, int64_t n, float eta, int64_t K_global,
+                     int32_t num_buckets, const int64_t *bucket_row_begin,
+                     const int64_t *bucket_K, const void *grad, int32_t grad_is_bf16,
+                     float *h, float *g, int32_t *idx, float *agg, int64_t *K_total,
+                     float *norms_out) {
+  if (N < 1 || d < 1 || n < 1 || idx == NULL || K_total == NULL) return 1;
+  const int64_t m = ceil_div(d, n);
+  if (m > INT32_MAX) return 1;
+  float *norms = norms_out ? norms_out : (float *)malloc((size_t)(N * m) * sizeof(float));
+  int rc = 1;
+  if (norms == NULL) return 1;
+  /* Validate the selection configuration (on zero keys) before the state. */
+  for (int64_t p = 0; p < m; ++p) norms[p] = 0.0f;
+  if (oracle_select(m, norms, K_global, num_buckets, bucket_row_begin, bucket_K, idx, K_total))
+    goto done;
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) goto done;
+#pragma omp parallel for schedule(static)
+  for (int64_t ip = 0; ip < (int64_t)N * m; ++ip) {
+    const int64_t i = ip / m, p = ip % m;
+    const int64_t len = p * n + n <= d ? n : d - p * n;
+    norms[ip] = row_norm2(h + i * d, g + i * d, p * n, len);
+  }
+  {
+    int64_t kt = 0;
+    for (int32_t i = 0; i < N; ++i) {
+      if (oracle_select(m, norms + (int64_t)i * m, K_global, num_buckets, bucket_row_begin,
+                        bucket_K, idx + (int64_t)i * *K_total, &kt))
+        goto done;
+    }
+  }
+  if (*K_total > 0 && agg == NULL) goto done;
+#pragma omp parallel for schedule(static)
+  for (int64_t iq = 0; iq < (int64_t)N * *K_total; ++iq) {
+    const int64_t i = iq / *K_total, p = idx[iq];
+    const int64_t len = p * n + n <= d ? n : d - p * n;
+    gather_own_row(h + i * d, g + i * d, p * n, len, n, agg + iq * n);
+  }
+  rc = 0;
+done:
+  if (!norms_out) free(norms);
+  return rc;
+}
+
+int oracle_step_topk_tensors(int32_t N, float eta, int32_t num_tensors, const int64_t *rows,
+                             const int64_t *cols, const int64_t *K, const void *grad,
+                             int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                             float *agg, int64_t *K_total, int64_t *agg_len,
+                             float *norms_out) {
+  int64_t d, m, *begin = NULL;
+  if (N < 1 || idx == NULL || K_total == NULL || agg_len == NULL) return 1;
+  if (tensor_buckets(num_tensors, rows, cols, K, &d, &m, &begin)) return 1;
+  float *norms = norms_out ? norms_out : (float *)malloc((size_t)(N * m) * sizeof(float));
+  int64_t *row_off = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *row_len = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *slot = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int rc = 1;
+  if (norms == NULL || row_off == NULL || row_len == NULL || slot == NULL) goto done;
+  /* Row p of tensor b starts at the tensor's offset + (p - row0_b) * cols_b. */
+  {
+    int64_t off = 0, p = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) {
+      for (int64_t r = 0; r < rows[b]; ++r, ++p) {
+        row_off[p] = off + r * cols[b];
+        row_len[p] = cols[b];
+      }
+      off += rows[b] * cols[b];
+    }
+  }
+  /* Validate the selection configuration (on zero keys) before the state. */
+  for (int64_t p = 0; p < m; ++p) norms[p] = 0.0f;
+  if (oracle_select(m, norms, 0, num_tensors, begin, K, idx, K_total)) goto done;
+  if (*K_total > 0 && agg == NULL) goto done;
+  /* Payload slot of output position q: tensors in order, K_b rows of cols_b. */
+  {
+    int64_t q = 0, a0 = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) {
+      const int64_t kb = K[b] < rows[b] ? K[b] : rows[b];
+      for (int64_t r = 0; r < kb; ++r, ++q, a0 += cols[b]) slot[q] = a0;
+    }
+    *agg_len = a0;
+  }
+  if (oracle_momentum(N, d, eta, grad, grad_is_bf16, h)) goto done;
+#pragma omp parallel for schedule(static)
+  for (int64_t ip = 0; ip < (int64_t)N * m; ++ip) {
+    const int64_t i = ip / m, p = ip % m;
+    norms[ip] = row_norm2(h + i * d, g + i * d, row_off[p], row_len[p]);
+  }
+  {
+    int64_t kt = 0;
+    for (int32_t i = 0; i < N; ++i)
+      if (oracle_select(m, norms + (int64_t)i * m, 0, num_tensors, begin, K,
+                        idx + (int64_t)i * *K_total, &kt))
+        goto done;
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t iq = 0; iq < (int64_t)N * *K_total; ++iq) {
+    const int64_t i = iq / *K_total, q = iq % *K_total, p = idx[iq];
+    gather_own_row(h + i * d, g + i * d, row_off[p], row_len[p], row_len[p],
+                   agg + i * *agg_len + slot[q]);
+  }
+  rc = 0;
+done:
+  if (!norms_out) free(norms);
+  free(row_off);
+  free(row_len);
+  free(slot);
+  free(begin);
+  return rc;
 }

@@ -118,6 +118,40 @@ int oracle_optimizer(int32_t optimizer, int32_t N, int64_t d, int64_t T,
                      float eps, float weight_decay, const float *G, float *x,
                      float *m, float *v);
 
+/* Comparison compressors of Table I inside the same EF21M step.
+ * Rand-K: K rows per bucket drawn uniformly (shared seed, unscaled); row p's
+ * key is (float)(SplitMix64 output t*m + p of the seed's stream >> 40), the K
+ * largest keys kept (ties to the lower row); payload summed over nodes as for
+ * ARC-Top-K.  keys_out ([m]) is optional. */
+int oracle_randk_keys(uint64_t seed, int64_t t, int64_t m, float *keys);
+int oracle_step_randk(int32_t N, int64_t d, int64_t n, float eta, uint64_t seed,
+                      int64_t t, int64_t K_global, int32_t num_buckets,
+                      const int64_t *bucket_row_begin, const int64_t *bucket_K,
+                      const void *grad, int32_t grad_is_bf16, float *h, float *g,
+                      int32_t *idx, float *agg, int64_t *K_total, float *keys_out);
+int oracle_step_randk_tensors(int32_t N, float eta, uint64_t seed, int64_t t,
+                              int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K, const void *grad,
+                              int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                              float *agg, int64_t *K_total, int64_t *agg_len,
+                              float *keys_out);
+
+/* Top-K (All-Gather): node i keeps its own K rows of largest ||Delta^(i)_p||^2
+ * (fmaf chain of squares, ascending columns, from +0; ties to the lower
+ * row).  idx is [N][K_total] (K_total per node), agg [N][L]: node i's rows of
+ * Delta^(i) (single view: K_total x n, +0 past d; tensors: packed), nothing
+ * summed; g^(i) += Delta^(i) on node i's rows.  norms_out ([N][m]) optional. */
+int oracle_step_topk(int32_t N, int64_t d, int64_t n, float eta, int64_t K_global,
+                     int32_t num_buckets, const int64_t *bucket_row_begin,
+                     const int64_t *bucket_K, const void *grad, int32_t grad_is_bf16,
+                     float *h, float *g, int32_t *idx, float *agg, int64_t *K_total,
+                     float *norms_out);
+int oracle_step_topk_tensors(int32_t N, float eta, int32_t num_tensors, const int64_t *rows,
+                             const int64_t *cols, const int64_t *K, const void *grad,
+                             int32_t grad_is_bf16, float *h, float *g, int32_t *idx,
+                             float *agg, int64_t *K_total, int64_t *agg_len,
+                             float *norms_out);
+
 /* Number of threads the oracle's parallel loops use. */
 int oracle_num_threads(void);
 
