@@ -37,17 +37,44 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w, K_total):
-    """Bytes the method must move per step (each array touched once)."""
+def algorithmic_bytes(w, K_total, compressor="arc"):
+    """Bytes the method must move per step (each array touched once).
+    sketch_kernel: the first (streaming) stage of the step."""
     bg = w.bytes_per_grad
     Nd = w.N * w.d
+    payload = w.payload_elems()
+    if compressor == "randk":
+        stream = Nd * (bg + 8)                      # grad + h read/write
+        keys = 4 * w.m                              # keys written
+        select = 4 * 4 * w.m
+        gather = payload * (12 * w.N + 4)
+        return {"sketch_kernel": stream, "step": stream + keys + select + gather + 4 * K_total}
+    if compressor == "topk":
+        stream = Nd * (bg + 12) + 4 * w.N * w.m     # + per-node row norms written
+        select = 4 * 4 * w.N * w.m
+        gather = payload * w.N * 16                 # h, g read, g written, values written
+        return {"sketch_kernel": stream, "step": stream + select + gather + 4 * K_total}
     stream = Nd * (bg + 12)                         # grad + h read/write + g read
     sketch_out = 4 * w.N * w.m * w.r                # per-worker sketch written
     reduce_ = 4 * w.N * w.m * w.r + 4 * w.m         # sketch read, importance written
     select = 4 * 4 * w.m                            # importance read by 4 passes
-    gather = w.payload_elems() * (12 * w.N + 4)     # h, g read, g written, agg written
+    gather = payload * (12 * w.N + 4)               # h, g read, g written, agg written
     return {"sketch_kernel": stream + sketch_out, "step": stream + sketch_out + reduce_ +
             select + gather + 4 * K_total}
+
+
+def table1_communication(w, comp, compressor):
+    """Values each node sends per step (Table I's column), from the actual
+    row counts: uncompressed 2mn (= 2d), ARC-Top-K 2Kn + 2mr, Rand-K 2Kn,
+    Top-K (N - 1)(nK + K) with an All-Gather of values and indices."""
+    if compressor == "topk":
+        K_node, L = comp.K_total // w.N, comp.payload // w.N
+        sent = (w.N - 1) * (L + K_node)
+    elif compressor == "randk":
+        sent = 2 * comp.payload
+    else:
+        sent = 2 * comp.payload + 2 * comp.m * w.r
+    return {"values": sent, "uncompressed": 2 * w.d, "fraction": sent / (2 * w.d)}
 
 
 def kernel_source_digest(path=KERNEL_SOURCE):
@@ -194,6 +221,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--compressor", default="arc", choices=["arc", "randk", "topk"],
+                    help="ARC-Top-K, or a comparison compressor of Table I in the same step")
     ap.add_argument("--batches", type=int, default=4,
                     help="distinct gradient batches kept resident and cycled")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -243,7 +272,7 @@ def main():
                               seed=w.sketch_seed, grad_dtype=w.grad_dtype,
                               buckets=w.buckets(),
                               tensors=w.tensor_views() if w.per_tensor else None,
-                              device=dev, stream=stream)
+                              compressor=args.compressor, device=dev, stream=stream)
         stream.synchronize()
         log(f"[bench] m={comp.m} K_total={comp.K_total}; {comp.describe()}; warmup {args.warmup}")
         for t in range(args.warmup):
@@ -264,14 +293,15 @@ def main():
         stage_ms, nsteps = arc.arc_timing_read(comp.ctx)
         arc.arc_timing_enable(comp.ctx, False)
         model = None
-        if not args.no_model_step:
+        if not args.no_model_step and args.compressor != "topk":
             model = model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb,
                                       args.warmup + args.steps)
     ms_per_step = total_ms / args.steps
     stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
     log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
 
-    byt = algorithmic_bytes(w, comp.K_total)
+    byt = algorithmic_bytes(w, comp.K_total, args.compressor)
+    comm = table1_communication(w, comp, args.compressor)
     sk_ms = stages["sketch"]
     achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
     traffic = kernel_traffic(w)
@@ -303,6 +333,7 @@ def main():
                    "K_rows": comp.K_total, "grad_dtype": w.grad_dtype, "eta": w.eta,
                    "mu": w.mu, "buckets": 0 if w.buckets() is None else len(w.buckets()[1]),
                    "view": "per_tensor" if w.per_tensor else "single",
+                   "compressor": args.compressor,
                    "tensors": len(w.views) if w.per_tensor else 0,
                    "payload_elems": comp.payload},
         "step_hbm_GBps": step_gbps,
@@ -311,9 +342,14 @@ def main():
         "path": comp_desc,
         "roofline": {
             "bound": "hbm",
-            "kernel": "sketch stage: sketch_fused_kernel launches (momentum + residual + "
-                      "sketch + worker sum + importance), plus the general-row kernels "
-                      "where the layout has any",
+            "kernel": {"arc": "sketch stage: sketch_per_worker_kernel (4 or more workers) "
+                              "or sketch_fused_kernel (fewer; also the worker sum and "
+                              "importance) launches, momentum + residual + sketch, plus the "
+                              "general-row kernels where the layout has any",
+                       "randk": "momentum_vec_kernel (Eq. (11a) over N*d)",
+                       "topk": "row-norm stage: sketch_per_worker_kernel in norm mode "
+                               "(momentum + residual + per-node squared row norms)",
+                       }[args.compressor],
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
@@ -324,6 +360,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "ef21m_iteration": model,
+        "communication_per_node": comm,
     }
     print(json.dumps(out), flush=True)
 

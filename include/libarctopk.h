@@ -67,6 +67,25 @@ typedef enum {
 
 typedef enum { ARC_DTYPE_F32 = 0, ARC_DTYPE_BF16 = 1 } arc_dtype;
 
+/*
+ * Compressor inside the EF21M step (Table I).  All keep K rows per bucket
+ * (or tensor) of Delta^(i) = h_t^(i) - g_{t-1}^(i) and move g^(i) by the kept
+ * rows (Eq. (11b)).
+ *   ARC_COMP_ARC    ARC-Top-K (Alg. 1): rows by the sketched importance,
+ *                   shared by every node; payload summed over nodes.
+ *   ARC_COMP_RANDK  Rand-K: rows drawn uniformly with the shared seed, the
+ *                   same on every node, unscaled; payload summed over nodes.
+ *                   Row p's key is (float)(x >> 40) for x the SplitMix64
+ *                   output number t*m + p of the stream seeded with `seed`;
+ *                   the K largest keys are kept, ties to the lower row.
+ *   ARC_COMP_TOPK   Top-K: every node its own K rows of largest ||Delta_p||^2
+ *                   (fmaf chain of squares over the row in ascending column
+ *                   order from +0, ties to the lower row); each node's rows
+ *                   and values are returned as they are (the All-Gather
+ *                   payload), nothing summed.
+ */
+typedef enum { ARC_COMP_ARC = 0, ARC_COMP_RANDK = 1, ARC_COMP_TOPK = 2 } arc_compressor;
+
 /* Largest projection dimension r accepted. */
 #define ARC_MAX_R 32
 
@@ -109,6 +128,8 @@ typedef struct {
  *                n, K and num_buckets must then be 0.  A tensor of width w
  *                uses the projection V_t of width w (tensors of equal width
  *                share it).  Host array, copied by arc_create.
+ *   compressor   arc_compressor (0 = ARC-Top-K); r and V are unused by
+ *                Rand-K and Top-K
  */
 typedef struct {
   int64_t d;
@@ -125,7 +146,7 @@ typedef struct {
   int32_t reserved; /* must be 0 */
   const arc_tensor *tensors;
   int32_t num_tensors;
-  int32_t reserved2; /* must be 0 */
+  int32_t compressor; /* arc_compressor */
 } arc_config;
 
 /*
@@ -143,14 +164,16 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  *   h        [N*d] binary32 momentum, read and written (Eq. (11a))
  *   g        [N*d] binary32 error-feedback state; rows in I are updated
  *            (Eq. (11b)), all other elements are left bit-for-bit unchanged
- *   out_idx  [K_total] int32: the selected rows, ascending within each bucket,
- *            buckets in order
+ *   out_idx  [arc_selected_rows(ctx)] int32: the selected rows, ascending
+ *            within each bucket, buckets in order
  *   out_agg  [arc_payload_elems(ctx)] binary32: the selected rows in
  *            out_idx order, each as sum_i Delta^(i) of that row (ascending
- *            worker order).  Single view: K_total rows of n values, +0 past
- *            d.  Per-tensor mode: packed, each row with its tensor's width.
- * K_total = arc_selected_rows(ctx).  out_idx / out_agg may be NULL only when
- * K_total == 0.  Pointers 16-byte aligned with d % 4 == 0 and row widths
+ *            worker order).  Single view: rows of n values, +0 past d.
+ *            Per-tensor mode: packed, each row with its tensor's width.
+ *   ARC_COMP_TOPK: out_idx is [N][K] (node i's rows at [i*K, (i+1)*K)) and
+ *            out_agg [N][L] (node i's rows of Delta^(i), laid out as above),
+ *            with K and L one node's row count and payload length.
+ * out_idx / out_agg may be NULL only when no row is kept.  Pointers 16-byte aligned with d % 4 == 0 and row widths
  * that are multiples of 32 take the vectorised path; anything else takes a
  * slower path with identical results.
  */
@@ -187,7 +210,8 @@ typedef struct {
 } arc_model_config;
 
 /*
- * One EF21M iteration (11a)-(11c) on the context's stream.
+ * One EF21M iteration (11a)-(11c) on the context's stream (ARC_COMP_ARC and
+ * ARC_COMP_RANDK; ARC_COMP_TOPK gives ARC_ERR_UNSUPPORTED).
  *   t < dense_steps: the identity compressor (no compression yet): for every
  *     coordinate, Eq. (11a), Delta_i = h_i - g_i, g_i = g_i + Delta_i, and
  *     G = G + (Delta_0 + Delta_1 + ...); out_idx and out_agg are not written.
@@ -214,7 +238,8 @@ arc_status arc_destroy(arc_ctx *ctx);
 /* Rows of the m x n view (m = ceil(d/n)); -1 for NULL. */
 int64_t arc_num_rows(const arc_ctx *ctx);
 
-/* Rows selected per step after clamping each K to its bucket; -1 for NULL. */
+/* Entries of out_idx per step: the rows kept after clamping each K to its
+ * bucket (N times that for ARC_COMP_TOPK, one list per node); -1 for NULL. */
 int64_t arc_selected_rows(const arc_ctx *ctx);
 
 /* Elements of out_agg per step; -1 for NULL. */

@@ -60,10 +60,12 @@ class arc_config(ctypes.Structure):
         ("reserved", ctypes.c_int32),
         ("tensors", ctypes.POINTER(arc_tensor)),
         ("num_tensors", ctypes.c_int32),
-        ("reserved2", ctypes.c_int32),
+        ("compressor", ctypes.c_int32),
     ]
 
 
+ARC_COMP_ARC, ARC_COMP_RANDK, ARC_COMP_TOPK = 0, 1, 2
+COMPRESSORS = {"arc": ARC_COMP_ARC, "randk": ARC_COMP_RANDK, "topk": ARC_COMP_TOPK}
 ARC_OPT_SGD, ARC_OPT_MSGD, ARC_OPT_ADAM = 0, 1, 2
 OPTIMIZERS = {"sgd": ARC_OPT_SGD, "msgd": ARC_OPT_MSGD, "adam": ARC_OPT_ADAM}
 
@@ -146,14 +148,14 @@ def _addr(x):
 
 def make_config(*, d: int, N: int, n: int = 0, r: int = 4, K: int = 0, eta: float,
                 seed: int, grad_dtype: int = ARC_DTYPE_F32, buckets=None, tensors=None,
-                reserved: int = 0, reserved2: int = 0):
+                reserved: int = 0, compressor=0):
     """Build an ``arc_config``; ``buckets`` = (row_begin[nb+1], K[nb]) or None;
     ``tensors`` = [(rows, cols, K), ...] for the per-tensor mode (then n, K
-    and buckets stay 0 / None).  Returns (config, keepalive) - keep the second
+    and buckets stay 0 / None); ``compressor`` = "arc", "randk" or "topk".  Returns (config, keepalive) - keep the second
     value alive until arc_create returns (it owns the arrays)."""
     cfg = arc_config(d=d, n=n, K=K, seed=seed & (2**64 - 1), N=N, r=r,
                      grad_dtype=grad_dtype, num_buckets=0, eta=eta, reserved=reserved,
-                     num_tensors=0, reserved2=reserved2)
+                     num_tensors=0, compressor=COMPRESSORS.get(compressor, compressor))
     keep = []
     if buckets is not None:
         begin, ks = buckets

@@ -43,6 +43,7 @@ arc_status fail_hip(hipError_t e, const char* where) {
   } while (0)
 
 constexpr int kEventsPerStep = 6;
+constexpr int32_t kPerWorkerFromWorkers = 4;  // see arc_ctx::use_fused
 constexpr int64_t kGroupRows = 64;  // rows of one row group (one wave's rows)
 constexpr int32_t kMaxTensors = 1 << 24;
 
@@ -80,7 +81,10 @@ struct arc_ctx {
   float eta = 0.f, a = 0.f;
   uint64_t seed = 0;
   bool tensor_mode = false;
-  int64_t K_total = 0, payload = 0;
+  int32_t compressor = ARC_COMP_ARC;
+  // Rows kept and payload floats per step, over all nodes (Top-K returns
+  // every node's rows; the others one shared list), and for one node.
+  int64_t K_total = 0, payload = 0, K_node = 0, payload_node = 0;
   std::vector<arc::BucketDesc> buckets;
   std::vector<arc::BlockDesc> blocks;
   // projection: one V_t per distinct row width, concatenated in first-use order
@@ -103,6 +107,7 @@ struct arc_ctx {
   float* S_dev = nullptr;
   float* sigma_dev = nullptr;
   arc::RowGroup* groups_dev = nullptr;
+  int32_t* sel_dev = nullptr;  // Top-K: selection over the N*m norms
   arc::GatherBucket* gather_dev = nullptr;
   arc::BucketDesc* buckets_dev = nullptr;
   arc::BlockDesc* blocks_dev = nullptr;
@@ -121,8 +126,14 @@ struct arc_ctx {
   std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
   size_t ev_used = 0;
 
-  bool fused_fits() const {
-    return N <= arc::kMaxFusedWorkers &&
+  // The fused sketch kernel streams the N workers' copies of the same rows
+  // in one block; the per-worker kernel streams consecutive row groups of
+  // one worker per block and leaves the worker sum to a small reduce kernel.
+  // Measured on one MI355X: with 2 workers fused is faster (7B layout 31.9
+  // vs 32.5 ms), with 4 the per-worker order is (1.1B 11.47 vs 11.7-11.85
+  // ms, per-tensor 1.1B 11.77 vs 12.37 ms), with 8 they tie (GPT-2 small).
+  bool use_fused() const {
+    return N < kPerWorkerFromWorkers && N <= arc::kMaxFusedWorkers &&
            arc::fused_sketch_lds_bytes(N) <= max_lds_per_block;
   }
 
@@ -148,6 +159,7 @@ struct arc_ctx {
     (void)hipStreamSynchronize(stream);
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
                     static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
+                    static_cast<void*>(sel_dev),
                     static_cast<void*>(gather_dev), static_cast<void*>(buckets_dev),
                     static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
                     static_cast<void*>(hist_dev), static_cast<void*>(blockcnt_dev)})
@@ -197,8 +209,9 @@ arc_status check_config(const arc_config* cfg, int64_t* m_out) {
   if (cfg->grad_dtype != ARC_DTYPE_F32 && cfg->grad_dtype != ARC_DTYPE_BF16)
     return fail(ARC_ERR_INVALID, "grad_dtype must be ARC_DTYPE_F32 or ARC_DTYPE_BF16");
   if (!(cfg->eta >= 0.0f && cfg->eta <= 1.0f)) return fail(ARC_ERR_INVALID, "eta must be in [0, 1]");
-  if (cfg->reserved != 0 || cfg->reserved2 != 0)
-    return fail(ARC_ERR_INVALID, "reserved fields must be 0");
+  if (cfg->reserved != 0) return fail(ARC_ERR_INVALID, "reserved must be 0");
+  if (cfg->compressor < ARC_COMP_ARC || cfg->compressor > ARC_COMP_TOPK)
+    return fail(ARC_ERR_INVALID, "compressor must be ARC_COMP_ARC, ARC_COMP_RANDK or ARC_COMP_TOPK");
   if (cfg->d > INT64_MAX / cfg->N) return fail(ARC_ERR_INVALID, "N*d overflows");
   if (cfg->num_tensors < 0) return fail(ARC_ERR_INVALID, "num_tensors must be >= 0");
   if (cfg->num_tensors > 0) return check_tensors(cfg, m_out);
@@ -309,10 +322,32 @@ void balance_for_xcds(std::vector<arc::RowGroup>* groups, int32_t group_rows) {
 // with balancing; TinyLlama (29,000) 11.87 ms without, 12.15 ms with it.
 constexpr size_t kBalanceBelowGroups = 64 * 256;
 
+// Selection buckets of one node's view (begin[0..nb], want[0..nb)).  Top-K
+// selects for every node separately over the N*m norms: node i's copies of
+// the buckets are offset by i*m rows.
+void build_node_selection(const std::vector<int64_t>& begin, const std::vector<int64_t>& want,
+                          arc_ctx* c) {
+  if (c->compressor != ARC_COMP_TOPK) {
+    build_selection_plan(begin, want, c);
+    c->K_node = c->K_total;
+    return;
+  }
+  std::vector<int64_t> all_begin{0}, all_want;
+  for (int32_t i = 0; i < c->N; ++i)
+    for (size_t b = 0; b + 1 < begin.size(); ++b) {
+      all_begin.push_back(static_cast<int64_t>(i) * c->m + begin[b + 1]);
+      all_want.push_back(want[b]);
+    }
+  build_selection_plan(all_begin, all_want, c);
+  c->K_node = c->K_total / c->N;
+}
+
 // Lowers the configuration to the kernels' tables (host side only).
 void build_plan(const arc_config* cfg, arc_ctx* c) {
   GroupLists lists;
   std::vector<int64_t> begin{0}, want;
+  // r in {1,2,4,8} for the vectorised sketch; the other compressors use no V.
+  const bool r_ok = c->compressor != ARC_COMP_ARC || vector_r(c->r);
   if (!c->tensor_mode) {
     // One m x n view (Eq. (3)); rows [0, m_full) are whole, row m_full (if
     // any) holds the d - m_full*n remaining coordinates.
@@ -320,7 +355,7 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
     c->v_off[c->n] = 0;
     c->v_floats = c->n * c->r;
     const int64_t m_full = c->d / c->n;
-    const int32_t gr = c->d % 4 == 0 && vector_r(c->r) ? vector_group_rows(c->n) : 0;
+    const int32_t gr = c->d % 4 == 0 && r_ok ? vector_group_rows(c->n) : 0;
     if (gr > 0) {
       add_groups(0, 0, m_full, c->n, c->n, 0, gr, &lists);
       if (c->m > m_full)
@@ -337,8 +372,26 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
         want.push_back(cfg->bucket_K[b]);
       }
     }
-    build_selection_plan(begin, want, c);
-    c->payload = c->K_total * c->n;
+    build_node_selection(begin, want, c);
+    c->payload_node = c->K_node * c->n;
+    // Top-K gathers each node's rows through bucket tables (both layouts).
+    int64_t work = 0;
+    for (size_t b = 0; b + 1 < begin.size(); ++b) {
+      const arc::BucketDesc& bd = c->buckets[b];
+      arc::GatherBucket gb{};
+      gb.row0 = bd.lo;
+      gb.elem_off = bd.lo * c->n;
+      gb.out_off = bd.out_off;
+      gb.agg_off = bd.out_off * c->n;
+      gb.work_off = work;
+      gb.rows = bd.hi - bd.lo;
+      gb.cols = static_cast<int32_t>(c->n);
+      gb.k = static_cast<int32_t>(bd.k);
+      gb.vec = c->n % 4 == 0 && c->d % 4 == 0;
+      if (c->compressor == ARC_COMP_TOPK) c->gather.push_back(gb);
+      work += bd.k * ((c->n + 3) / 4);
+    }
+    c->gather_work = c->compressor == ARC_COMP_TOPK ? work : 0;
   } else {
     // One view per tensor; tensors of equal width share one V_t.
     for (int32_t b = 0; b < cfg->num_tensors; ++b) {
@@ -351,15 +404,14 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
     int64_t off = 0, row0 = 0;
     for (int32_t b = 0; b < cfg->num_tensors; ++b) {
       const arc_tensor& t = cfg->tensors[b];
-      const int32_t gr =
-          off % 4 == 0 && c->d % 4 == 0 && vector_r(c->r) ? vector_group_rows(t.cols) : 0;
+      const int32_t gr = off % 4 == 0 && c->d % 4 == 0 && r_ok ? vector_group_rows(t.cols) : 0;
       add_groups(off, row0, t.rows, t.cols, t.cols, c->v_off[t.cols], gr, &lists);
       off += t.rows * t.cols;
       row0 += t.rows;
       begin.push_back(row0);
       want.push_back(t.K);
     }
-    build_selection_plan(begin, want, c);
+    build_node_selection(begin, want, c);
     int64_t agg_off = 0, work = 0;
     off = 0;
     for (int32_t b = 0; b < cfg->num_tensors; ++b) {
@@ -380,9 +432,11 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
       work += bd.k * ((t.cols + 3) / 4);
       off += t.rows * t.cols;
     }
-    c->payload = agg_off;
+    c->payload_node = agg_off;
     c->gather_work = work;
   }
+  const int64_t nodes = c->compressor == ARC_COMP_TOPK ? c->N : 1;
+  c->payload = nodes * c->payload_node;
   c->groups.clear();
   for (int sz = 0; sz < 3; ++sz) {
     if (c->tensor_mode && lists.vec[sz].size() < kBalanceBelowGroups)
@@ -472,12 +526,15 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   int64_t m = 0;
   arc_status st = check_config(cfg, &m);
   if (st != ARC_OK) return st;
+  if (cfg->compressor == ARC_COMP_TOPK && m > INT32_MAX / cfg->N)
+    return fail(ARC_ERR_INVALID, "Top-K: N * m must be below 2^31");
 
   arc_ctx* c = new (std::nothrow) arc_ctx();
   if (c == nullptr) return fail(ARC_ERR_NOMEM, "host allocation failed");
   try {
     c->d = cfg->d;
     c->tensor_mode = cfg->num_tensors > 0;
+    c->compressor = cfg->compressor;
     c->n = c->tensor_mode ? 0 : cfg->n;
     c->m = m;
     c->N = cfg->N;
@@ -516,7 +573,9 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
       (st = dev_alloc(&c->state_dev, nb, "hipMalloc(state)")) ||
       (st = dev_alloc(&c->hist_dev, arc::kRadixPasses * nb * arc::kRadixBins,
                       "hipMalloc(hist)")) ||
-      (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")))
+      (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")) ||
+      (st = dev_alloc(&c->sel_dev, c->compressor == ARC_COMP_TOPK ? c->K_total : 0,
+                      "hipMalloc(selection)")))
     return bail(st);
   for (int s = 0; s < 2; ++s) {
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
@@ -589,7 +648,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   // are 16-byte aligned; otherwise every group takes the general kernel.
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
   const int64_t nvec = aligned16(grad) && aligned16(h) && aligned16(g) ? c->nvec_groups : 0;
-  const bool fused = nvec > 0 && c->fused_fits();
+  const bool fused = nvec > 0 && c->use_fused();
 
   size_t slot = 0;
   if (c->timing) {
@@ -602,41 +661,80 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   }
   arc_status st;
   if ((st = record(c, slot, 0))) return st;
-  if ((st = upload_projection(c, t))) return st;
+  if (c->compressor == ARC_COMP_ARC && (st = upload_projection(c, t))) return st;
   if ((st = record(c, slot, 1))) return st;
-  // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
-  // the fused kernel also forms the worker sum and importance of its rows.
-  // One launch per group size present (64, 32, 16 rows).
-  for (int sz = 0, first = 0; nvec > 0 && sz < 3; first += c->vec_count[sz], ++sz) {
-    const int32_t gr = 64 >> sz;
-    const arc::RowGroup* grp = c->groups_dev + first;
-    if (fused) {
-      ARC_HIP(arc::launch_sketch_fused(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
-                                       c->vec_count[sz], c->S_dev, c->sigma_dev, c->d, c->m,
-                                       c->N, c->r, c->eta, c->a, c->stream),
-              "fused sketch launch");
-    } else {
-      ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
-                                            c->vec_count[sz], c->S_dev, c->d, c->m, c->N, c->r,
-                                            c->eta, c->a, c->stream),
-              "sketch launch");
-    }
-  }
-  ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
-                                     ngroups - nvec, c->S_dev, c->d, c->m, c->N, c->r, c->eta,
-                                     c->a, c->stream),
-          "sketch launch (general rows)");
-  if ((st = record(c, slot, 2))) return st;
-  // Stage 1: worker sum + importance of the rows the fused kernel did not do.
-  const int64_t done = fused ? nvec : 0;
-  ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + done,
-                                        ngroups - done, c->m, c->N, c->r, c->stream),
-          "reduce launch");
-  if ((st = record(c, slot, 3))) return st;
-  // Stage 2: per-bucket top-K.
   const arc::SelectWorkspace ws = c->select_ws();
-  ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
-  if ((st = record(c, slot, 4))) return st;
+  if (c->compressor == ARC_COMP_RANDK) {
+    // Stage 0: Eq. (11a) alone (the residual is needed at the kept rows only).
+    const bool vec = (c->N * c->d) % 4 == 0 && aligned16(grad) && aligned16(h);
+    ARC_HIP(arc::launch_momentum(vec, grad, c->grad_bf16, h, c->N * c->d, c->eta, c->a,
+                                 c->stream),
+            "momentum launch");
+    if ((st = record(c, slot, 2))) return st;
+    // Stage 1: the shared random keys; stage 2: their per-bucket top-K.
+    ARC_HIP(arc::launch_randk_keys(c->seed, t, c->m, c->sigma_dev, c->stream), "keys launch");
+    if ((st = record(c, slot, 3))) return st;
+    ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
+    if ((st = record(c, slot, 4))) return st;
+  } else if (c->compressor == ARC_COMP_TOPK) {
+    // Stage 0: Eq. (11a) with every node's squared row norms of Delta.
+    for (int sz = 0, first = 0; nvec > 0 && sz < 3; first += c->vec_count[sz], ++sz)
+      ARC_HIP(arc::launch_row_norms(64 >> sz, grad, c->grad_bf16, h, g, c->V_dev,
+                                    c->groups_dev + first, c->vec_count[sz], c->S_dev, c->d,
+                                    c->m, c->N, c->eta, c->a, c->stream),
+              "row norm launch");
+    ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
+                                       ngroups - nvec, c->S_dev, c->d, c->m, c->N, 1, c->eta,
+                                       c->a, true, c->stream),
+            "row norm launch (general rows)");
+    if ((st = record(c, slot, 2))) return st;
+    if ((st = record(c, slot, 3))) return st;
+    // Stage 2: every node's own top-K over its norms.
+    ARC_HIP(arc::launch_select(c->S_dev, ws, c->sel_dev, c->stream), "select launch");
+    if ((st = record(c, slot, 4))) return st;
+    // Stage 3: every node's rows, unsummed (the All-Gather payload).
+    const bool vec = c->d % 4 == 0 && c->payload_node % 4 == 0 && aligned16(h) &&
+                     aligned16(g) && aligned16(out_agg);
+    ARC_HIP(arc::launch_topk_gather(h, g, c->sel_dev, out_idx, out_agg, c->gather_dev,
+                                    static_cast<int32_t>(c->gather.size()), c->gather_work,
+                                    c->K_node, c->payload_node, c->d, c->m, c->N, vec,
+                                    c->stream),
+            "gather launch");
+    return record(c, slot, 5);
+  } else {
+    // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
+    // the fused kernel also forms the worker sum and importance of its rows.
+    // One launch per group size present (64, 32, 16 rows).
+    for (int sz = 0, first = 0; nvec > 0 && sz < 3; first += c->vec_count[sz], ++sz) {
+      const int32_t gr = 64 >> sz;
+      const arc::RowGroup* grp = c->groups_dev + first;
+      if (fused) {
+        ARC_HIP(arc::launch_sketch_fused(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
+                                         c->vec_count[sz], c->S_dev, c->sigma_dev, c->d, c->m,
+                                         c->N, c->r, c->eta, c->a, c->stream),
+                "fused sketch launch");
+      } else {
+        ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
+                                              c->vec_count[sz], c->S_dev, c->d, c->m, c->N,
+                                              c->r, c->eta, c->a, c->stream),
+                "sketch launch");
+      }
+    }
+    ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
+                                       ngroups - nvec, c->S_dev, c->d, c->m, c->N, c->r, c->eta,
+                                       c->a, false, c->stream),
+            "sketch launch (general rows)");
+    if ((st = record(c, slot, 2))) return st;
+    // Stage 1: worker sum + importance of the rows the fused kernel did not do.
+    const int64_t done = fused ? nvec : 0;
+    ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + done,
+                                          ngroups - done, c->m, c->N, c->r, c->stream),
+            "reduce launch");
+    if ((st = record(c, slot, 3))) return st;
+    // Stage 2: per-bucket top-K.
+    ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
+    if ((st = record(c, slot, 4))) return st;
+  }
   // Stage 3: gather + worker sum + error-feedback update.
   const bool G_ok = G == nullptr || aligned16(G);
   if (c->tensor_mode) {
@@ -673,6 +771,8 @@ arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, con
                           float* h, float* g, float* G, float* x, float* opt_m, float* opt_v,
                           int32_t* out_idx, float* out_agg) {
   if (mc == nullptr) return fail(ARC_ERR_INVALID, "model config is NULL");
+  if (c != nullptr && c->compressor == ARC_COMP_TOPK)
+    return fail(ARC_ERR_UNSUPPORTED, "arc_model_step: Top-K payloads are not merged into G");
   // A dense iteration writes no payload, so out_idx / out_agg may be NULL.
   const bool dense = t < mc->dense_steps;
   arc_status st = check_step_args(c, t, grad, h, g, out_idx, out_agg, !dense);
@@ -749,17 +849,22 @@ arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, con
 arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
   if (c == nullptr || buf == nullptr || len <= 0) return fail(ARC_ERR_INVALID, "NULL argument");
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
-  const char* sketch = c->nvec_groups == 0 ? "general"
-                       : c->fused_fits()   ? "fused"
-                                           : "per_worker+reduce";
+  const char* comp = c->compressor == ARC_COMP_RANDK  ? "randk"
+                     : c->compressor == ARC_COMP_TOPK ? "topk"
+                                                      : "arc";
+  const char* sketch = c->compressor == ARC_COMP_RANDK ? "none"
+                       : c->nvec_groups == 0           ? "general"
+                       : c->compressor == ARC_COMP_TOPK ? "row_norms"
+                       : c->use_fused()                ? "fused"
+                                                       : "per_worker+reduce";
   int radix = 0;
   for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
   std::snprintf(buf, static_cast<size_t>(len),
-                "mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
+                "compressor=%s mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
                 "(64:%lld 32:%lld 16:%lld rows) general_groups=%lld fused_lds_bytes=%zu "
                 "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld "
                 "payload=%lld",
-                c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
+                comp, c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
                 static_cast<long long>(ngroups), static_cast<long long>(c->nvec_groups),
                 static_cast<long long>(c->vec_count[0]), static_cast<long long>(c->vec_count[1]),
                 static_cast<long long>(c->vec_count[2]),

@@ -118,11 +118,38 @@ hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_
                                     float a, hipStream_t stream);
 
 // The same for any row group (any width, r <= ARC_MAX_R, element alignment,
-// ragged last row), one wave per (group, worker).
+// ragged last row), one wave per (group, worker).  norm (r = 1): S holds each
+// row's squared norm of Delta instead of its sketch.
 hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
                                  const float* g, const float* V, const RowGroup* groups,
                                  int64_t ngroups, float* S, int64_t d, int64_t m, int32_t N,
-                                 int32_t r, float eta, float a, hipStream_t stream);
+                                 int32_t r, float eta, float a, bool norm, hipStream_t stream);
+
+// Momentum + residual + per-worker squared row norms of Delta into
+// norms[N][m] (Top-K), vectorisable groups as for launch_sketch_per_worker.
+hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_bf16, float* h,
+                            const float* g, const float* V, const RowGroup* groups,
+                            int64_t ngroups, float* norms, int64_t d, int64_t m, int32_t N,
+                            float eta, float a, hipStream_t stream);
+
+// ---- comparison compressors (arc_compare.hip) ----
+
+// Eq. (11a) alone over all N*d coordinates (Rand-K needs no residual pass).
+hipError_t launch_momentum(bool vec, const void* grad, int32_t grad_bf16, float* h,
+                           int64_t count, float eta, float a, hipStream_t stream);
+
+// Rand-K keys of rows [0, m) at step t: (float)(SplitMix64(seed, t*m + p) >> 40).
+hipError_t launch_randk_keys(uint64_t seed, int64_t t, int64_t m, float* keys,
+                             hipStream_t stream);
+
+// Top-K gather: work item w in [0, N*work) is node w / work's item w % work of
+// the bucket table; sel holds the selection over the N*m norms (node i's rows
+// offset by i*m).  Writes node i's local rows to out_idx[i*K_total + q], its
+// rows of Delta to agg[i*payload + ...] (+0 past d), g^(i) += Delta there.
+hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int32_t* out_idx,
+                              float* agg, const GatherBucket* buckets, int32_t nb,
+                              int64_t work, int64_t K_total, int64_t payload, int64_t d,
+                              int64_t m, int32_t N, bool vec, hipStream_t stream);
 
 // P = sum_i S[i] (ascending i), sigma = row norm squared of P, for the rows
 // of groups[0 .. ngroups).

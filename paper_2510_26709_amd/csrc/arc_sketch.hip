@@ -38,8 +38,9 @@ constexpr int kTileF4 = 576;  // >= G * (512 / G + 1) for every G
 // three streams are read through buffer resources that end at the group's
 // last row, so in a group of fewer than G rows the missing rows read as zero
 // and are not stored.  Lanes G..63 repeat the chains of lanes 0..G-1; the
-// caller keeps only lanes below the group's row count.
-template <int R, bool BF16, int G>
+// caller keeps only lanes below the group's row count.  NORM (R = 1): the
+// chain is the row's squared norm, fmaf(Delta, Delta, s), and V is unused.
+template <int R, bool BF16, int G, bool NORM = false>
 __device__ __forceinline__ void sketch_rows(
     const void* __restrict__ grad, float* __restrict__ h,
     const float* __restrict__ g, const float* __restrict__ V, int64_t d,
@@ -127,9 +128,13 @@ __device__ __forceinline__ void sketch_rows(
       const float e4[4] = {dv.x, dv.y, dv.z, dv.w};
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
+        if constexpr (NORM) {
+          s[0] = fmaf(e4[jj], e4[jj], s[0]);
+        } else {
 #pragma unroll
-        for (int k = 0; k < R; ++k)
-          s[k] = fmaf(e4[jj], Vc[(q * 4 + jj) * R + k], s[k]);
+          for (int k = 0; k < R; ++k)
+            s[k] = fmaf(e4[jj], Vc[(q * 4 + jj) * R + k], s[k]);
+        }
       }
     }
     wave_lds_fence();
@@ -189,7 +194,7 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
 // ---------------------------------------------------------------------------
 constexpr int kSketchWaves = 4;
 
-template <int R, bool BF16, int G>
+template <int R, bool BF16, int G, bool NORM = false>
 __global__ void __launch_bounds__(kSketchWaves * kWave)
 sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
                          const float* __restrict__ g, const float* __restrict__ V,
@@ -204,7 +209,7 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   if (gi >= ngroups) return;  // whole wave; no block barrier follows
   const RowGroup grp = groups[gi];
   float s[R];
-  sketch_rows<R, BF16, G>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
+  sketch_rows<R, BF16, G, NORM>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
   if (lane < grp.rows) {
     float* out = S + ((int64_t)i * m + grp.row0 + lane) * R;
 #pragma unroll
@@ -328,6 +333,32 @@ hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_
   if (!dispatch<PerWorkerLaunch>(r, grad_bf16 != 0, group_rows, grad, h, g, V, groups,
                                  ngroups, S, d, m, N, eta, a, stream))
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_bf16, float* h,
+                            const float* g, const float* V, const RowGroup* groups, int64_t ngroups,
+                            float* norms, int64_t d, int64_t m, int32_t N, float eta, float a,
+                            hipStream_t stream) {
+  if (ngroups <= 0) return hipSuccess;
+  const dim3 grid(blocks_for(ngroups, kSketchWaves), (unsigned)N), block(kSketchWaves * kWave);
+#define ARC_NORM_CASE(GG)                                                                    \
+  case GG:                                                                                   \
+    if (grad_bf16)                                                                           \
+      hipLaunchKernelGGL((sketch_per_worker_kernel<1, true, GG, true>), grid, block, 0,      \
+                         stream, grad, h, g, V, groups, ngroups, norms, d, m, eta, a);       \
+    else                                                                                     \
+      hipLaunchKernelGGL((sketch_per_worker_kernel<1, false, GG, true>), grid, block, 0,     \
+                         stream, grad, h, g, V, groups, ngroups, norms, d, m, eta, a);       \
+    break;
+  switch (group_rows) {
+    ARC_NORM_CASE(64)
+    ARC_NORM_CASE(32)
+    ARC_NORM_CASE(16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef ARC_NORM_CASE
   return hipGetLastError();
 }
 

@@ -24,12 +24,14 @@ constexpr int kGenChunk = 32;       // columns per chunk
 constexpr int kGenPitch = kGenChunk + 1;  // LDS row pitch (floats), conflict-free row reads
 constexpr int kGenRowsPerPass = 16;  // rows loaded per pass: 8 instructions x 2 rows
 
+// norm != 0 (r = 1): the chain is the row's squared norm, fmaf(Delta, Delta,
+// s), for the Top-K comparison compressor; V is unused.
 template <bool BF16>
 __global__ void __launch_bounds__(kWave)
 sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
                       const float* __restrict__ g, const float* __restrict__ V,
                       const RowGroup* __restrict__ groups, float* __restrict__ S,
-                      int64_t d, int64_t m, int32_t r, float eta, float a) {
+                      int64_t d, int64_t m, int32_t r, float eta, float a, int32_t norm) {
   __shared__ float tile[kWave * kGenPitch];
   extern __shared__ float acc[];  // [r][64] partial sums
   const RowGroup grp = groups[blockIdx.x];
@@ -86,7 +88,7 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
         float s = acc[k * kWave + lane];
 #pragma unroll 8
         for (int j = 0; j < cw; ++j) {
-          const float t = fmaf(row[j], Vc[j * r + k], s);
+          const float t = fmaf(row[j], norm ? row[j] : Vc[j * r + k], s);
           s = j < jn ? t : s;
         }
         acc[k * kWave + lane] = s;
@@ -105,17 +107,17 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
 hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
                                  const float* g, const float* V, const RowGroup* groups,
                                  int64_t ngroups, float* S, int64_t d, int64_t m, int32_t N,
-                                 int32_t r, float eta, float a, hipStream_t stream) {
+                                 int32_t r, float eta, float a, bool norm, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
   if (r < 1 || r > ARC_MAX_R) return hipErrorInvalidValue;
   const dim3 grid((unsigned)ngroups, (unsigned)N), block(kWave);
   const size_t lds = sizeof(float) * kWave * r;
   if (grad_bf16)
     hipLaunchKernelGGL(sketch_general_kernel<true>, grid, block, lds, stream, grad, h, g, V,
-                       groups, S, d, m, r, eta, a);
+                       groups, S, d, m, r, eta, a, norm ? 1 : 0);
   else
     hipLaunchKernelGGL(sketch_general_kernel<false>, grid, block, lds, stream, grad, h, g, V,
-                       groups, S, d, m, r, eta, a);
+                       groups, S, d, m, r, eta, a, norm ? 1 : 0);
   return hipGetLastError();
 }
 

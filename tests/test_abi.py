@@ -142,7 +142,7 @@ TBASE = dict(d=64 * 96 + 300, N=2, r=4, eta=0.1, seed=1,
     dict(n=96),                                    # n with tensors
     dict(K=3),                                     # global K with tensors
     dict(buckets=([0, 65], [1])),                  # buckets with tensors
-    dict(reserved2=1),
+    dict(compressor=3),
     dict(tensors=[(2**40, 2**40, 1)], d=2**40),   # rows*cols would overflow int64
 ])
 def test_create_rejects_invalid_tensor_config(override):

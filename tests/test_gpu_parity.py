@@ -55,6 +55,15 @@ CASES = [
                               family=1)),
     ("generic_wide_ragged", dict(d=1000 * 70 + 999, N=3, n=1000, r=4, K=5, steps=2)),
     ("generic_many_workers", dict(d=50 * 257, N=11, n=50, r=4, K=20, steps=2)),
+    # fused kernel (N <= 3) and per-worker kernel (N >= 4) for every r and
+    # row-group size (16 rows for n % 128 == 0, 32 for n % 64, 64 otherwise)
+    ("fused_r2_g64", dict(d=96 * 513, N=2, n=96, r=2, K=7, steps=2)),
+    ("fused_g32_bf16", dict(d=192 * 400, N=3, n=192, r=4, K=9, steps=2, grad_dtype="bf16",
+                            family=1)),
+    ("per_worker_g32", dict(d=192 * 500, N=4, n=192, r=4, K=9, steps=2)),
+    ("per_worker_r8_g64", dict(d=32 * 4097, N=4, n=32, r=8, K=100, steps=2)),
+    ("per_worker_r1_bf16", dict(d=128 * 777, N=5, n=128, r=1, K=30, steps=2, grad_dtype="bf16",
+                                family=1)),
 ]
 
 
@@ -65,7 +74,8 @@ def test_parity_small(name, kw):
 
 
 def test_describe_names_the_kernel_path():
-    for N, want in ((4, "sketch=fused"), (8, "sketch=fused"), (12, "sketch=per_worker+reduce")):
+    for N, want in ((2, "sketch=fused"), (3, "sketch=fused"), (4, "sketch=per_worker+reduce"),
+                    (8, "sketch=per_worker+reduce"), (12, "sketch=per_worker+reduce")):
         comp = arc.Compressor(d=256 * 64, N=N, n=256, K=3, eta=0.1, seed=1)
         try:
             desc = comp.describe()
