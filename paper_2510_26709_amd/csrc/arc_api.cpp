@@ -95,7 +95,7 @@ struct arc_ctx {
   // the general ones
   std::vector<arc::RowGroup> groups;
   int64_t nvec_groups = 0;
-  std::array<int64_t, 3> vec_count{};  // groups of 64, 32 and 16 rows
+  std::array<int64_t, 4> vec_count{};  // groups of 64, 32, 16 and 8 rows
   // per-tensor gather
   std::vector<arc::GatherBucket> gather;
   int64_t gather_work = 0;
@@ -272,10 +272,12 @@ void build_selection_plan(const std::vector<int64_t>& begin, const std::vector<i
 }
 
 struct GroupLists {
-  std::vector<arc::RowGroup> vec[3], general;  // vec: 64, 32, 16 rows
+  std::vector<arc::RowGroup> vec[4], general;  // vec: 64, 32, 16, 8 rows
 };
 
-int size_slot(int32_t group_rows) { return group_rows == 64 ? 0 : group_rows == 32 ? 1 : 2; }
+int size_slot(int32_t group_rows) {
+  return group_rows == 64 ? 0 : group_rows == 32 ? 1 : group_rows == 16 ? 2 : 3;
+}
 
 // Row groups over `rows` rows of width `cols` that start at coordinate
 // elem_off and global row row0; the last row holds last_len <= cols values.
@@ -438,7 +440,7 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
   const int64_t nodes = c->compressor == ARC_COMP_TOPK ? c->N : 1;
   c->payload = nodes * c->payload_node;
   c->groups.clear();
-  for (int sz = 0; sz < 3; ++sz) {
+  for (int sz = 0; sz < 4; ++sz) {
     if (c->tensor_mode && lists.vec[sz].size() < kBalanceBelowGroups)
       balance_for_xcds(&lists.vec[sz], 64 >> sz);
     c->vec_count[sz] = static_cast<int64_t>(lists.vec[sz].size());
@@ -678,7 +680,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
     if ((st = record(c, slot, 4))) return st;
   } else if (c->compressor == ARC_COMP_TOPK) {
     // Stage 0: Eq. (11a) with every node's squared row norms of Delta.
-    for (int sz = 0, first = 0; nvec > 0 && sz < 3; first += c->vec_count[sz], ++sz)
+    for (int sz = 0, first = 0; nvec > 0 && sz < 4; first += c->vec_count[sz], ++sz)
       ARC_HIP(arc::launch_row_norms(64 >> sz, grad, c->grad_bf16, h, g, c->V_dev,
                                     c->groups_dev + first, c->vec_count[sz], c->S_dev, c->d,
                                     c->m, c->N, c->eta, c->a, c->stream),
@@ -705,7 +707,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
     // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
     // the fused kernel also forms the worker sum and importance of its rows.
     // One launch per group size present (64, 32, 16 rows).
-    for (int sz = 0, first = 0; nvec > 0 && sz < 3; first += c->vec_count[sz], ++sz) {
+    for (int sz = 0, first = 0; nvec > 0 && sz < 4; first += c->vec_count[sz], ++sz) {
       const int32_t gr = 64 >> sz;
       const arc::RowGroup* grp = c->groups_dev + first;
       if (fused) {
@@ -861,13 +863,13 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
   for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
   std::snprintf(buf, static_cast<size_t>(len),
                 "compressor=%s mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
-                "(64:%lld 32:%lld 16:%lld rows) general_groups=%lld fused_lds_bytes=%zu "
+                "(64:%lld 32:%lld 16:%lld 8:%lld rows) general_groups=%lld fused_lds_bytes=%zu "
                 "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld "
                 "payload=%lld",
                 comp, c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
                 static_cast<long long>(ngroups), static_cast<long long>(c->nvec_groups),
                 static_cast<long long>(c->vec_count[0]), static_cast<long long>(c->vec_count[1]),
-                static_cast<long long>(c->vec_count[2]),
+                static_cast<long long>(c->vec_count[2]), static_cast<long long>(c->vec_count[3]),
                 static_cast<long long>(ngroups - c->nvec_groups),
                 arc::fused_sketch_lds_bytes(c->N), c->max_lds_per_block, c->buckets.size(),
                 radix, c->blocks.size(), static_cast<long long>(c->K_total),

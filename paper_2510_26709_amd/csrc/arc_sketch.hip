@@ -15,15 +15,15 @@
 namespace arc {
 namespace {
 
-// Row groups of G in {64, 32, 16} rows.  One 16-byte load instruction of a
-// wave covers G/8 rows of LPR = 512/G lanes each, so eight instructions cover
-// the group's G rows over a chunk of CW = 4*LPR columns (32, 64 or 128).  The
+// Row groups of G in {64, 32, 16, 8} rows.  One 16-byte load instruction of
+// a wave covers G/8 rows of LPR = 512/G lanes each, so eight instructions
+// cover the group's G rows over a chunk of CW = 4*LPR columns (32 to 256).  The
 // LDS tile holds G rows of Delta with LPR float4 per row plus one float4 of
 // padding (at most 576 float4 for every G), so that consecutive lanes reading
 // consecutive rows hit distinct 16-byte bank groups.
 template <int G>
 struct GroupShape {
-  static_assert(G == 64 || G == 32 || G == 16, "row group of 64, 32 or 16 rows");
+  static_assert(G == 64 || G == 32 || G == 16 || G == 8, "row group of 64 to 8 rows");
   static constexpr int kLanesPerRow = 512 / G;
   static constexpr int kRowsPerLoad = kWave / kLanesPerRow;
   static constexpr int kChunkCols = 4 * kLanesPerRow;
@@ -73,8 +73,12 @@ __device__ __forceinline__ void sketch_rows(
 
   const uint32_t nchunks = n / kCW;
   uint2 x_next[8];  // bf16, 64-row groups: this lane's grad of the next chunk
-  for (uint32_t c = 0; c < nchunks; ++c) {
-    float4 xv[8], hv[8], gv[8];
+  // Loads of chunk c into xv, hv, gv (off[] at chunk c).  The loop issues
+  // the next chunk's loads as soon as this chunk's momentum has consumed the
+  // registers, so they are in flight while this chunk's chains run.  bf16
+  // gradients stay packed in xv.x, xv.y until used.
+  float4 xv[8], hv[8], gv[8];
+  auto issue_loads = [&](uint32_t c) {
     const bool even = (c & 1) == 0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -90,26 +94,32 @@ __device__ __forceinline__ void sketch_rows(
         } else {
           w = x_next[u];
         }
-        xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
+        xv[u] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), 0.f, 0.f);
       } else if constexpr (BF16) {
         // 32 or more lanes per row: each load already covers whole lines.
         const uint2 w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
-        xv[u] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
+        xv[u] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), 0.f, 0.f);
       } else {
         xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, off[u]);
       }
       hv[u] = buffer_load_f4<kCacheDefault>(rh, off[u]);
       gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, off[u]);
     }
-    // Keep all loads of the chunk in flight before the first use.
-    __builtin_amdgcn_sched_barrier(0);
+  };
+  if (nchunks > 0) issue_loads(0);
+  for (uint32_t c = 0; c < nchunks; ++c) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
+      float4 x4 = xv[u];
+      if constexpr (BF16) {
+        const uint32_t w0 = __float_as_uint(xv[u].x), w1 = __float_as_uint(xv[u].y);
+        x4 = make_float4(bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1));
+      }
       float4 hn;
-      hn.x = fmaf(eta, xv[u].x, a * hv[u].x);
-      hn.y = fmaf(eta, xv[u].y, a * hv[u].y);
-      hn.z = fmaf(eta, xv[u].z, a * hv[u].z);
-      hn.w = fmaf(eta, xv[u].w, a * hv[u].w);
+      hn.x = fmaf(eta, x4.x, a * hv[u].x);
+      hn.y = fmaf(eta, x4.y, a * hv[u].y);
+      hn.z = fmaf(eta, x4.z, a * hv[u].z);
+      hn.w = fmaf(eta, x4.w, a * hv[u].w);
       if (u * kRPL + sub < rows) buffer_store_f4<kCacheNonTemporal>(rh, off[u], hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
@@ -119,6 +129,9 @@ __device__ __forceinline__ void sketch_rows(
       tile[(u * kRPL + sub) * kPitch + quad] = dl;
       off[u] += kCW * 4;
     }
+    // The next chunk's loads go out before this chunk's chains run.
+    if (c + 1 < nchunks) issue_loads(c + 1);
+    __builtin_amdgcn_sched_barrier(0);
     wave_lds_fence();
     const float* Vc = V + c * kCW * R;
     const float4* my_row = tile + (lane & (G - 1)) * kPitch;
@@ -287,6 +300,7 @@ bool dispatch_g(int32_t group_rows, Args... args) {
     case 64: Launch<R, BF16, 64>::run(args...); return true;
     case 32: Launch<R, BF16, 32>::run(args...); return true;
     case 16: Launch<R, BF16, 16>::run(args...); return true;
+    case 8: Launch<R, BF16, 8>::run(args...); return true;
     default: return false;
   }
 }
@@ -355,6 +369,7 @@ hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_b
     ARC_NORM_CASE(64)
     ARC_NORM_CASE(32)
     ARC_NORM_CASE(16)
+    ARC_NORM_CASE(8)
     default:
       return hipErrorInvalidValue;
   }
