@@ -31,6 +31,16 @@ struct GroupShape {
 };
 constexpr int kTileF4 = 576;  // >= G * (512 / G + 1) for every G
 
+// After its tile, a wave's LDS holds the projection rows of the current
+// chunk (CW x R binary32), so that the chains read V from LDS: wave-uniform
+// scalar loads of V would share the lgkm counter with the tile reads, and a
+// wait for one would be a wait for both.
+template <int R, int G, bool NORM>
+constexpr int slice_f4() { return NORM ? 0 : GroupShape<G>::kChunkCols * R / 4; }
+template <int R, int G, bool NORM>
+constexpr int wave_lds_f4() { return kTileF4 + slice_f4<R, G, NORM>(); }
+constexpr int kMaxWaveLdsF4 = kTileF4 + 512;  // largest slice: R = 8, G = 8
+
 // One wave's pass over the rows of one row group of worker i: loads the
 // grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
 // writes h back, parks Delta in LDS, then runs this lane's r chains over its
@@ -47,6 +57,8 @@ __device__ __forceinline__ void sketch_rows(
     const RowGroup& grp, int32_t i, float eta, float a, float4* tile,
     float (&s)[R]) {
   using Shape = GroupShape<G>;
+  constexpr int kSliceF4 = slice_f4<R, G, NORM>();
+  constexpr int kSliceRegs = (kSliceF4 + kWave - 1) / kWave;
   constexpr int kLPR = Shape::kLanesPerRow;
   constexpr int kRPL = Shape::kRowsPerLoad;
   constexpr int kCW = Shape::kChunkCols;
@@ -78,8 +90,16 @@ __device__ __forceinline__ void sketch_rows(
   // registers, so they are in flight while this chunk's chains run.  bf16
   // gradients stay packed in xv.x, xv.y until used.
   float4 xv[8], hv[8], gv[8];
+  float4 vreg[kSliceRegs > 0 ? kSliceRegs : 1];  // this lane's share of chunk c's V rows
+  float4* vslice = tile + kTileF4;
   auto issue_loads = [&](uint32_t c) {
     const bool even = (c & 1) == 0;
+    if constexpr (kSliceF4 > 0) {
+      const float4* src = reinterpret_cast<const float4*>(V + (size_t)c * kCW * R);
+#pragma unroll
+      for (int r4 = 0; r4 < kSliceRegs; ++r4)
+        if (lane + r4 * kWave < kSliceF4) vreg[r4] = src[lane + r4 * kWave];
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if constexpr (BF16 && G == 64) {
@@ -129,11 +149,16 @@ __device__ __forceinline__ void sketch_rows(
       tile[(u * kRPL + sub) * kPitch + quad] = dl;
       off[u] += kCW * 4;
     }
+    if constexpr (kSliceF4 > 0) {
+#pragma unroll
+      for (int r4 = 0; r4 < kSliceRegs; ++r4)
+        if (lane + r4 * kWave < kSliceF4) vslice[lane + r4 * kWave] = vreg[r4];
+    }
     // The next chunk's loads go out before this chunk's chains run.
     if (c + 1 < nchunks) issue_loads(c + 1);
     __builtin_amdgcn_sched_barrier(0);
     wave_lds_fence();
-    const float* Vc = V + c * kCW * R;
+    const float* Vc = reinterpret_cast<const float*>(vslice);
     const float4* my_row = tile + (lane & (G - 1)) * kPitch;
 #pragma unroll
     for (int q = 0; q < kLPR; ++q) {
@@ -169,11 +194,12 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
                     const RowGroup* __restrict__ groups, float* __restrict__ S,
                     float* __restrict__ sigma, int64_t d, int64_t m, int32_t N,
                     float eta, float a) {
-  extern __shared__ float4 lds_tiles[];  // N tiles of kTileF4
+  extern __shared__ float4 lds_tiles[];  // N wave areas of wave_lds_f4 float4
+  constexpr int kWaveF4 = wave_lds_f4<R, G, false>();
   const int lane = threadIdx.x & (kWave - 1);
   const int i = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // worker
   const RowGroup grp = groups[xcd_contiguous_block(blockIdx.x, gridDim.x)];
-  float4* tile = lds_tiles + i * kTileF4;
+  float4* tile = lds_tiles + i * kWaveF4;
   float s[R];
   sketch_rows<R, BF16, G>(grad, h, g, V, d, grp, i, eta, a, tile, s);
   const bool mine = lane < grp.rows;
@@ -194,7 +220,7 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
 #pragma unroll
     for (int k = 0; k < R; ++k) {
       float P = s[k];
-      for (int32_t w = 1; w < N; ++w) P = P + base[w * kTileF4 * 4 + k * kWave + lane];
+      for (int32_t w = 1; w < N; ++w) P = P + base[w * kWaveF4 * 4 + k * kWave + lane];
       acc = fmaf(P, P, acc);
     }
     sigma[p] = acc;
@@ -214,7 +240,7 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
                          const RowGroup* __restrict__ groups, int64_t ngroups,
                          float* __restrict__ S, int64_t d, int64_t m, float eta,
                          float a) {
-  __shared__ float4 tiles[kSketchWaves][kTileF4];
+  __shared__ float4 tiles[kSketchWaves][wave_lds_f4<R, G, NORM>()];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t i = blockIdx.y;
@@ -266,7 +292,7 @@ reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
 }  // namespace
 
 size_t fused_sketch_lds_bytes(int32_t N) {
-  return (size_t)N * kTileF4 * sizeof(float4);
+  return (size_t)N * kMaxWaveLdsF4 * sizeof(float4);
 }
 
 namespace {
@@ -276,9 +302,10 @@ struct FusedLaunch {
   static void run(const void* grad, float* h, const float* g, const float* V,
                   const RowGroup* groups, int64_t ngroups, float* S, float* sigma,
                   int64_t d, int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
+    constexpr size_t kWaveBytes = wave_lds_f4<R, G, false>() * sizeof(float4);
     hipLaunchKernelGGL((sketch_fused_kernel<R, BF16, G>), dim3((unsigned)ngroups),
-                       dim3(N * kWave), fused_sketch_lds_bytes(N), stream, grad, h, g, V,
-                       groups, S, sigma, d, m, N, eta, a);
+                       dim3(N * kWave), N * kWaveBytes, stream, grad, h, g, V, groups, S,
+                       sigma, d, m, N, eta, a);
   }
 };
 
