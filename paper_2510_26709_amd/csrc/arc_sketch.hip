@@ -40,6 +40,7 @@ constexpr int slice_f4() { return NORM ? 0 : GroupShape<G>::kChunkCols * R / 4; 
 template <int R, int G, bool NORM>
 constexpr int wave_lds_f4() { return kTileF4 + slice_f4<R, G, NORM>(); }
 constexpr int kMaxWaveLdsF4 = kTileF4 + 512;  // largest slice: R = 8, G = 8
+constexpr uint32_t kDropOffset = 0x80000000u;  // beyond every buffer resource here
 
 // One wave's pass over the rows of one row group of worker i: loads the
 // grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
@@ -90,15 +91,26 @@ __device__ __forceinline__ void sketch_rows(
   // registers, so they are in flight while this chunk's chains run.  bf16
   // gradients stay packed in xv.x, xv.y until used.
   float4 xv[8], hv[8], gv[8];
-  float4 vreg[kSliceRegs > 0 ? kSliceRegs : 1];  // this lane's share of chunk c's V rows
+  using VRegs = float __attribute__((ext_vector_type(4 * (kSliceRegs > 0 ? kSliceRegs : 1))));
+  VRegs vreg;  // this lane's share of chunk c's V rows
   float4* vslice = tile + kTileF4;
-  auto issue_loads = [&](uint32_t c) {
+  // Float4 of the slice that this lane moves for register r4; lanes past the
+  // slice's end repeat its last float4 (same value, same address), so that
+  // neither the load nor the store needs a branch.
+  auto slice_at = [&](int r4) { return min(lane + r4 * kWave, kSliceF4 - 1); };
+  auto issue_loads = [&](uint32_t c) __attribute__((always_inline)) {
     const bool even = (c & 1) == 0;
     if constexpr (kSliceF4 > 0) {
       const float4* src = reinterpret_cast<const float4*>(V + (size_t)c * kCW * R);
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
-        if (lane + r4 * kWave < kSliceF4) vreg[r4] = src[lane + r4 * kWave];
+      {
+        const float4 t = src[slice_at(r4)];
+        vreg[4 * r4] = t.x;
+        vreg[4 * r4 + 1] = t.y;
+        vreg[4 * r4 + 2] = t.z;
+        vreg[4 * r4 + 3] = t.w;
+      }
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -140,7 +152,11 @@ __device__ __forceinline__ void sketch_rows(
       hn.y = fmaf(eta, x4.y, a * hv[u].y);
       hn.z = fmaf(eta, x4.z, a * hv[u].z);
       hn.w = fmaf(eta, x4.w, a * hv[u].w);
-      if (u * kRPL + sub < rows) buffer_store_f4<kCacheNonTemporal>(rh, off[u], hn);
+      // Rows past the group's end get an offset far outside the resource, so
+      // the hardware drops their store: a select rather than a branch, which
+      // would make the compiler's wait counts for the loads in flight
+      // conservative on every path.
+      buffer_store_f4<kCacheNonTemporal>(rh, u * kRPL + sub < rows ? off[u] : kDropOffset, hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
@@ -152,7 +168,8 @@ __device__ __forceinline__ void sketch_rows(
     if constexpr (kSliceF4 > 0) {
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
-        if (lane + r4 * kWave < kSliceF4) vslice[lane + r4 * kWave] = vreg[r4];
+        vslice[slice_at(r4)] =
+            make_float4(vreg[4 * r4], vreg[4 * r4 + 1], vreg[4 * r4 + 2], vreg[4 * r4 + 3]);
     }
     // The next chunk's loads go out before this chunk's chains run.
     if (c + 1 < nchunks) issue_loads(c + 1);
