@@ -61,15 +61,19 @@ bool aligned16(const void* p) {
 bool vector_r(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8; }
 
 // Rows per group of the vectorised sketch kernels for a view of width cols,
-// or 0 when the width needs the general kernel.  Fewer rows per group give
-// more, shorter waves (the chunk widens instead); a width must be a whole
-// number of chunks, and a group small enough for 32-bit byte offsets.
+// or 0 when the width needs the general kernel (not a multiple of 4, or a
+// group too large for 32-bit byte offsets).  Fewer rows per group give more,
+// shorter waves (the chunk widens instead): the first size whose chunk
+// divides the width, else the one with the widest chunk that fits in a row
+// (each row's last chunk is then partial).
 constexpr int32_t kGroupSizes[] = {16, 32, 64};
 int32_t vector_group_rows(int64_t cols) {
-  if (cols > (int64_t{1} << 22)) return 0;
+  if (cols > (int64_t{1} << 22) || cols % 4 != 0) return 0;
   for (int32_t gr : kGroupSizes)
     if (cols % arc::vector_chunk_cols(gr) == 0) return gr;
-  return 0;
+  for (int32_t gr : kGroupSizes)
+    if (cols >= arc::vector_chunk_cols(gr)) return gr;
+  return kGroupSizes[2];
 }
 
 }  // namespace
@@ -308,7 +312,7 @@ void balance_for_xcds(std::vector<arc::RowGroup>* groups, int32_t group_rows) {
   std::vector<arc::RowGroup> sorted = *groups;
   std::stable_sort(sorted.begin(), sorted.end(),
                    [&](const arc::RowGroup& x, const arc::RowGroup& y) {
-                     return x.cols / chunk > y.cols / chunk;
+                     return (x.cols + chunk - 1) / chunk > (y.cols + chunk - 1) / chunk;
                    });
   constexpr int64_t kXcds = 8;
   const int64_t total = static_cast<int64_t>(sorted.size()), per = total / kXcds;
@@ -360,8 +364,10 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
     const int32_t gr = c->d % 4 == 0 && r_ok ? vector_group_rows(c->n) : 0;
     if (gr > 0) {
       add_groups(0, 0, m_full, c->n, c->n, 0, gr, &lists);
-      if (c->m > m_full)
-        add_groups(m_full * c->n, m_full, 1, c->n, c->d - m_full * c->n, 0, 0, &lists);
+      // The ragged row (a multiple of 4 values, as d and n are) is a
+      // one-row group as wide as its values.
+      const int64_t tail = c->d - m_full * c->n;
+      if (tail > 0) add_groups(m_full * c->n, m_full, 1, tail, tail, 0, gr, &lists);
     } else {
       add_groups(0, 0, c->m, c->n, c->d - (c->m - 1) * c->n, 0, 0, &lists);
     }

@@ -45,12 +45,15 @@ constexpr uint32_t kDropOffset = 0x80000000u;  // beyond every buffer resource h
 // One wave's pass over the rows of one row group of worker i: loads the
 // grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
 // writes h back, parks Delta in LDS, then runs this lane's r chains over its
-// row.  Local row l of the group starts at coordinate elem_off + l*n.  The
-// three streams are read through buffer resources that end at the group's
-// last row, so in a group of fewer than G rows the missing rows read as zero
-// and are not stored.  Lanes G..63 repeat the chains of lanes 0..G-1; the
-// caller keeps only lanes below the group's row count.  NORM (R = 1): the
-// chain is the row's squared norm, fmaf(Delta, Delta, s), and V is unused.
+// row.  Local row l of the group starts at coordinate elem_off + l*n; n is a
+// multiple of 4 but need not be one of the chunk width, in which case each
+// row's last chunk is partial: its lanes past the row's end load and store
+// nothing, and the chains stop at the row's end.  The three streams are read
+// through buffer resources that end at the group's last row, so in a group
+// of fewer than G rows the missing rows read as zero and are not stored.
+// Lanes G..63 repeat the chains of lanes 0..G-1; the caller keeps only lanes
+// below the group's row count.  NORM (R = 1): the chain is the row's squared
+// norm, fmaf(Delta, Delta, s), and V is unused.
 template <int R, bool BF16, int G, bool NORM = false>
 __device__ __forceinline__ void sketch_rows(
     const void* __restrict__ grad, float* __restrict__ h,
@@ -84,7 +87,15 @@ __device__ __forceinline__ void sketch_rows(
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
 
-  const uint32_t nchunks = n / kCW;
+  const uint32_t nchunks = (n + kCW - 1) / kCW;
+  // Columns of the last chunk: kCW unless the width is not a multiple of it.
+  const uint32_t tail = n - (nchunks - 1) * kCW;
+  const bool in_tail = (uint32_t)quad * 4 < tail;
+  // Offset o of this lane's access in chunk c, or kDropOffset (the hardware
+  // drops the access) where the lane is past the end of a partial last chunk.
+  auto col_off = [&](uint32_t o, uint32_t c) {
+    return c + 1 < nchunks || in_tail ? o : kDropOffset;
+  };
   uint2 x_next[8];  // bf16, 64-row groups: this lane's grad of the next chunk
   // Loads of chunk c into xv, hv, gv (off[] at chunk c).  The loop issues
   // the next chunk's loads as soon as this chunk's momentum has consumed the
@@ -94,10 +105,14 @@ __device__ __forceinline__ void sketch_rows(
   using VRegs = float __attribute__((ext_vector_type(4 * (kSliceRegs > 0 ? kSliceRegs : 1))));
   VRegs vreg;  // this lane's share of chunk c's V rows
   float4* vslice = tile + kTileF4;
-  // Float4 of the slice that this lane moves for register r4; lanes past the
-  // slice's end repeat its last float4 (same value, same address), so that
-  // neither the load nor the store needs a branch.
-  auto slice_at = [&](int r4) { return min(lane + r4 * kWave, kSliceF4 - 1); };
+  // Float4 of chunk c's slice that this lane moves for register r4; lanes
+  // past the slice's end (shorter in a partial last chunk, whose V rows end
+  // with the width's) repeat its last float4 (same value, same address), so
+  // that neither the load nor the store needs a branch.
+  auto slice_at = [&](int r4, uint32_t c) {
+    const int last = c + 1 < nchunks ? kSliceF4 - 1 : (int)(tail * R / 4) - 1;
+    return min(lane + r4 * kWave, last);
+  };
   auto issue_loads = [&](uint32_t c) __attribute__((always_inline)) {
     const bool even = (c & 1) == 0;
     if constexpr (kSliceF4 > 0) {
@@ -105,7 +120,7 @@ __device__ __forceinline__ void sketch_rows(
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
       {
-        const float4 t = src[slice_at(r4)];
+        const float4 t = src[slice_at(r4, c)];
         vreg[4 * r4] = t.x;
         vreg[4 * r4 + 1] = t.y;
         vreg[4 * r4 + 2] = t.z;
@@ -114,28 +129,29 @@ __device__ __forceinline__ void sketch_rows(
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
+      const uint32_t o = col_off(off[u], c);
       if constexpr (BF16 && G == 64) {
         // A row's bf16 grad for two consecutive 32-column chunks is one
         // 128-byte line; both 8-byte halves are requested together on even
         // chunks, so the line is fetched once rather than once per chunk.
         uint2 w;
         if (even) {
-          w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
+          w = buffer_load_u2<kCacheDefault>(rx, o / 2);
           if (c + 1 < nchunks)
-            x_next[u] = buffer_load_u2<kCacheDefault>(rx, off[u] / 2 + kCW * 2);
+            x_next[u] = buffer_load_u2<kCacheDefault>(rx, col_off(off[u] + kCW * 4, c + 1) / 2);
         } else {
           w = x_next[u];
         }
         xv[u] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), 0.f, 0.f);
       } else if constexpr (BF16) {
         // 32 or more lanes per row: each load already covers whole lines.
-        const uint2 w = buffer_load_u2<kCacheDefault>(rx, off[u] / 2);
+        const uint2 w = buffer_load_u2<kCacheDefault>(rx, o / 2);
         xv[u] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), 0.f, 0.f);
       } else {
-        xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, off[u]);
+        xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, o);
       }
-      hv[u] = buffer_load_f4<kCacheDefault>(rh, off[u]);
-      gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, off[u]);
+      hv[u] = buffer_load_f4<kCacheDefault>(rh, o);
+      gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, o);
     }
   };
   if (nchunks > 0) issue_loads(0);
@@ -156,7 +172,8 @@ __device__ __forceinline__ void sketch_rows(
       // the hardware drops their store: a select rather than a branch, which
       // would make the compiler's wait counts for the loads in flight
       // conservative on every path.
-      buffer_store_f4<kCacheNonTemporal>(rh, u * kRPL + sub < rows ? off[u] : kDropOffset, hn);
+      buffer_store_f4<kCacheNonTemporal>(rh, u * kRPL + sub < rows ? col_off(off[u], c) : kDropOffset,
+                                         hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
@@ -168,7 +185,7 @@ __device__ __forceinline__ void sketch_rows(
     if constexpr (kSliceF4 > 0) {
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
-        vslice[slice_at(r4)] =
+        vslice[slice_at(r4, c)] =
             make_float4(vreg[4 * r4], vreg[4 * r4 + 1], vreg[4 * r4 + 2], vreg[4 * r4 + 3]);
     }
     // The next chunk's loads go out before this chunk's chains run.
@@ -177,18 +194,32 @@ __device__ __forceinline__ void sketch_rows(
     wave_lds_fence();
     const float* Vc = reinterpret_cast<const float*>(vslice);
     const float4* my_row = tile + (lane & (G - 1)) * kPitch;
+    if (c + 1 < nchunks || tail == kCW) {
 #pragma unroll
-    for (int q = 0; q < kLPR; ++q) {
-      const float4 dv = my_row[q];
-      const float e4[4] = {dv.x, dv.y, dv.z, dv.w};
+      for (int q = 0; q < kLPR; ++q) {
+        const float4 dv = my_row[q];
+        const float e4[4] = {dv.x, dv.y, dv.z, dv.w};
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
+        for (int jj = 0; jj < 4; ++jj) {
+          if constexpr (NORM) {
+            s[0] = fmaf(e4[jj], e4[jj], s[0]);
+          } else {
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+              s[k] = fmaf(e4[jj], Vc[(q * 4 + jj) * R + k], s[k]);
+          }
+        }
+      }
+    } else {
+      // Partial last chunk: the chains end with the row's last column.
+      const float* rowf = reinterpret_cast<const float*>(my_row);
+      for (uint32_t j = 0; j < tail; ++j) {
+        const float e = rowf[j];
         if constexpr (NORM) {
-          s[0] = fmaf(e4[jj], e4[jj], s[0]);
+          s[0] = fmaf(e, e, s[0]);
         } else {
 #pragma unroll
-          for (int k = 0; k < R; ++k)
-            s[k] = fmaf(e4[jj], Vc[(q * 4 + jj) * R + k], s[k]);
+          for (int k = 0; k < R; ++k) s[k] = fmaf(e, Vc[j * R + k], s[k]);
         }
       }
     }

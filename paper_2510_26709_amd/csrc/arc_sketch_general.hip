@@ -6,10 +6,11 @@
 // One wave per (row group, worker).  Each 32-column chunk of the group's
 // 64 x 32 tile is loaded with one element per lane (two rows of 32 columns
 // per instruction, coalesced), 24 loads in flight per pass of 16 rows; Delta
-// goes to LDS, then lane p runs its row's r chains over the chunk in
-// ascending column order, its partial sums kept in LDS between chunks.  The
-// arithmetic is the same as the vectorised kernels', in the same order, so
-// both produce the same bits.
+// goes to LDS, and so do the chunk's 32 rows of V (transposed to [k][j]).
+// Lane p then runs its row's r chains over the chunk in ascending column
+// order, its partial sums kept in LDS between chunks.  The arithmetic is the
+// same as the vectorised kernels', in the same order, so both produce the
+// same bits.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -33,7 +34,9 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
                       const RowGroup* __restrict__ groups, float* __restrict__ S,
                       int64_t d, int64_t m, int32_t r, float eta, float a, int32_t norm) {
   __shared__ float tile[kWave * kGenPitch];
-  extern __shared__ float acc[];  // [r][64] partial sums
+  extern __shared__ float dyn[];
+  float* acc = dyn;              // [r][64] partial sums
+  float* vl = dyn + r * kWave;   // [r][32] this chunk's rows of V
   const RowGroup grp = groups[blockIdx.x];
   const int lane = threadIdx.x;
   const int32_t i = blockIdx.y;
@@ -45,8 +48,16 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
   const int cl = lane & (kGenChunk - 1);  // column within the chunk
   for (int32_t k = 0; k < r; ++k) acc[k * kWave + lane] = 0.0f;
 
-  for (int64_t c0 = 0; c0 < n; c0 += kGenChunk) {
-    const int cw = (int)(n - c0 < kGenChunk ? n - c0 : kGenChunk);
+  // A one-row group holds only the last row's values (a ragged tail row).
+  const int64_t span = rows == 1 ? grp.last_len : n;
+  for (int64_t c0 = 0; c0 < span; c0 += kGenChunk) {
+    const int cw = (int)(span - c0 < kGenChunk ? span - c0 : kGenChunk);
+    if (!norm) {
+      for (int t = lane; t < r * kGenChunk; t += kWave) {
+        const int k = t / kGenChunk, j = t - k * kGenChunk;
+        vl[t] = Vg[(c0 + (j < cw ? j : cw - 1)) * r + k];
+      }
+    }
     for (int pass = 0; pass * kGenRowsPerPass < rows; ++pass) {
       float xv[8], hv[8], gv[8];
       bool ok[8];
@@ -77,18 +88,21 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
     wave_lds_fence();
     {
       // This row's columns in the chunk: fewer in a ragged last row.  The
-      // column loop runs to the chunk width for every lane, so that V is
-      // read as wave-uniform scalars; the lane keeps only its first jn
+      // column loop runs to the chunk width for every lane (V's reads are
+      // wave-uniform LDS broadcasts); the lane keeps only its first jn
       // products.  Lanes at or past the row count compute unused values.
       const int64_t len = lane == rows - 1 ? grp.last_len : n;
       const int jn = (int)(len - c0 < cw ? (len - c0 > 0 ? len - c0 : 0) : cw);
       const float* row = tile + lane * kGenPitch;
-      const float* Vc = Vg + c0 * r;
+      float dl[kGenChunk];
+#pragma unroll
+      for (int j = 0; j < kGenChunk; ++j) dl[j] = row[j];
       for (int32_t k = 0; k < r; ++k) {
         float s = acc[k * kWave + lane];
-#pragma unroll 8
-        for (int j = 0; j < cw; ++j) {
-          const float t = fmaf(row[j], norm ? row[j] : Vc[j * r + k], s);
+        const float* vk = vl + k * kGenChunk;
+#pragma unroll
+        for (int j = 0; j < kGenChunk; ++j) {
+          const float t = fmaf(dl[j], norm ? dl[j] : vk[j], s);
           s = j < jn ? t : s;
         }
         acc[k * kWave + lane] = s;
@@ -111,7 +125,7 @@ hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
   if (ngroups <= 0) return hipSuccess;
   if (r < 1 || r > ARC_MAX_R) return hipErrorInvalidValue;
   const dim3 grid((unsigned)ngroups, (unsigned)N), block(kWave);
-  const size_t lds = sizeof(float) * kWave * r;
+  const size_t lds = sizeof(float) * (kWave + kGenChunk) * r;
   if (grad_bf16)
     hipLaunchKernelGGL(sketch_general_kernel<true>, grid, block, lds, stream, grad, h, g, V,
                        groups, S, d, m, r, eta, a, norm ? 1 : 0);

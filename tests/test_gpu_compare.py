@@ -60,6 +60,7 @@ def run_compare_case(*, compressor, d, N, n=0, tensors=None, K=0, buckets=None, 
 
 
 MIXED = [(70, 147, 9), (1, 64, 1), (129, 64, 4), (40, 512, 3), (2, 2, 2), (200, 96, 7)]
+PARTIAL = [(70, 100, 9), (1, 1000, 1), (33, 36, 3), (5, 4, 2), (129, 200, 4), (64, 96, 5)]
 
 CASES = [
     ("fast_f32_ragged", dict(d=256 * 700 + 40, N=3, n=256, K=9, steps=3)),
@@ -73,6 +74,9 @@ CASES = [
     ("tensors_mixed", dict(d=sum(a * b for a, b, _ in MIXED), N=3, tensors=MIXED)),
     ("tensors_bf16", dict(d=sum(a * b for a, b, _ in MIXED), N=2, tensors=MIXED,
                           grad_dtype="bf16", family=1)),
+    ("partial_chunks_per_worker", dict(d=1000 * 60 + 996, N=5, n=1000, K=7)),
+    ("tensors_partial_bf16", dict(d=sum(a * b for a, b, _ in PARTIAL), N=3, tensors=PARTIAL,
+                                  grad_dtype="bf16", family=1)),
 ]
 
 

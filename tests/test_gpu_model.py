@@ -81,6 +81,7 @@ def run_model_case(*, d, N, n=0, tensors=None, r=4, K=0, eta=0.1, seed=3, grad_d
 
 
 MIXED = [(70, 147, 9), (1, 64, 1), (129, 64, 4), (40, 512, 3), (2, 2, 2)]
+PARTIAL = [(70, 100, 9), (1, 1000, 1), (33, 36, 3), (5, 4, 2), (129, 200, 4)]
 
 CASES = [
     ("sgd_f32", dict(d=256 * 300, N=4, n=256, K=9, optimizer="sgd", lr=0.5)),
@@ -96,6 +97,8 @@ CASES = [
                            steps=3)),
     ("msgd_no_dense", dict(d=256 * 64, N=5, n=256, K=4, optimizer="msgd", dense_steps=0)),
     ("adam_per_worker_N12", dict(d=256 * 100, N=12, n=256, K=6, optimizer="adam")),
+    ("msgd_partial_chunk_tensors", dict(d=sum(a * b for a, b, _ in PARTIAL), N=4,
+                                        tensors=PARTIAL, optimizer="msgd")),
 ]
 
 

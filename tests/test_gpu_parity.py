@@ -64,6 +64,16 @@ CASES = [
     ("per_worker_r8_g64", dict(d=32 * 4097, N=4, n=32, r=8, K=100, steps=2)),
     ("per_worker_r1_bf16", dict(d=128 * 777, N=5, n=128, r=1, K=30, steps=2, grad_dtype="bf16",
                                 family=1)),
+    # widths that are multiples of 4 but not of the chunk: every row's last
+    # chunk is partial (32 + 4, 64 + 36, 7 x 128 + 104 columns), and the
+    # ragged tail row is a one-row vector group as wide as its values
+    ("partial_chunk_g64_bf16_fused", dict(d=36 * 900 + 20, N=2, n=36, r=8, K=40, steps=2,
+                                          grad_dtype="bf16", family=1)),
+    ("partial_chunk_g32_fused", dict(d=100 * 321 + 8, N=3, n=100, r=4, K=12, steps=3)),
+    ("partial_chunk_g16_bf16_per_worker", dict(d=1000 * 80 + 996, N=4, n=1000, r=4, K=5, steps=2,
+                                               grad_dtype="bf16", family=1)),
+    ("partial_chunk_n4_per_worker", dict(d=4 * 5000, N=5, n=4, r=2, K=60, steps=2)),
+    ("ragged_tail_r1_per_worker", dict(d=512 * 300 + 12, N=6, n=512, r=1, K=9, steps=2)),
 ]
 
 
@@ -86,6 +96,14 @@ def test_describe_names_the_kernel_path():
     comp = arc.Compressor(d=100 * 64, N=2, n=100, r=3, K=3, eta=0.1, seed=1)
     try:
         assert "sketch=general" in comp.describe()
+    finally:
+        comp.close()
+    # a width that is a multiple of 4 but of no chunk width, with a ragged
+    # tail row: all vector groups, no general kernel
+    comp = arc.Compressor(d=100 * 64 + 8, N=2, n=100, r=4, K=3, eta=0.1, seed=1)
+    try:
+        desc = comp.describe()
+        assert "sketch=fused" in desc and "general_groups=0" in desc, desc
     finally:
         comp.close()
 

@@ -34,6 +34,11 @@ ALIGNED = [(200, 96, 7), (1, 96, 1), (130, 256, 10), (64, 64, 64), (5, 32, 0), (
 MIXED = [(70, 147, 9), (3, 33, 1), (64, 96, 5), (1, 7, 1), (129, 64, 4), (1, 64, 1),
          (77, 160, 77), (2, 2, 5)]
 
+# Widths that are multiples of 4 but not of any chunk width: vector groups
+# whose rows end in a partial chunk (16-, 32- and 64-row groups).
+PARTIAL = [(70, 100, 9), (1, 1000, 1), (33, 36, 3), (5, 4, 2), (129, 200, 4), (2, 520, 1),
+           (64, 96, 5), (300, 44, 11)]
+
 
 def _random_layout(seed, count, max_rows=300):
     rng = np.random.default_rng(seed)
@@ -64,6 +69,11 @@ CASES = [
     ("mixed_bf16_N2", dict(tensors=MIXED, N=2, r=4, steps=2, grad_dtype="bf16", family=1)),
     ("mixed_r3_general", dict(tensors=MIXED, N=3, r=3, steps=2)),
     ("mixed_per_worker_N12", dict(tensors=MIXED, N=12, r=4, steps=2)),
+    ("partial_f32_N3", dict(tensors=PARTIAL, N=3, r=4, steps=3)),
+    ("partial_bf16_per_worker_N4", dict(tensors=PARTIAL, N=4, r=4, steps=2, grad_dtype="bf16",
+                                        family=1)),
+    ("partial_r8_N2", dict(tensors=PARTIAL, N=2, r=8, steps=2)),
+    ("partial_r1_bf16_N7", dict(tensors=PARTIAL, N=7, r=1, steps=2, grad_dtype="bf16", family=1)),
     ("one_tensor_multiblock_select", dict(tensors=[(40_000, 32, 9_000)], N=2, r=4, steps=2)),
     ("single_one_row_tensor", dict(tensors=[(1, 4096, 1)], N=2, r=4, steps=2)),
     ("all_k_zero", dict(tensors=[(64, 64, 0), (10, 32, 0)], N=2, r=4, steps=2)),
