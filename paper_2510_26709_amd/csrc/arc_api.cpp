@@ -15,7 +15,10 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <memory>
 #include <new>
+#include <stdexcept>
+#include <thread>
 #include <string>
 #include <vector>
 
@@ -118,13 +121,17 @@ struct arc_ctx {
   arc::BucketState* state_dev = nullptr;
   uint32_t* hist_dev = nullptr;
   uint32_t* blockcnt_dev = nullptr;
-  // projection staging: two pinned buffers, reused every other step
+  // projection staging: two pinned buffers, reused every other step; the
+  // pool fills the next step's buffer while the device runs this step
   float* V_pinned[2] = {nullptr, nullptr};
   hipEvent_t V_done[2] = {nullptr, nullptr};
   bool V_pending[2] = {false, false};
   int V_slot = 0;
   std::vector<float> V_override;
   bool use_override = false;
+  std::vector<arc::ProjectionBlock> V_blocks;
+  std::unique_ptr<arc::ProjectionPool> V_pool;
+  int64_t V_prefetch_t = -1;  // step whose V_t the pool put in V_pinned[V_slot]
   // stage timing
   bool timing = false;
   std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
@@ -160,6 +167,7 @@ struct arc_ctx {
   }
 
   void release() {
+    V_pool.reset();  // joins the threads before their buffers go
     (void)hipStreamSynchronize(stream);
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
                     static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
@@ -480,25 +488,54 @@ arc_status record(arc_ctx* c, size_t slot, int which) {
   return ARC_OK;
 }
 
-// Pinned staging + async copy of this step's projections.
-arc_status upload_projection(arc_ctx* c, int64_t t) {
-  const int s = c->V_slot;
-  c->V_slot ^= 1;
+// Host threads for the projection: one per 16K values (a few hundred
+// microseconds of Box-Muller each), at most 8 and at most half the cores.
+int projection_threads(int64_t v_floats) {
+  const int64_t by_size = 1 + v_floats / 16384;
+  const int64_t cores = static_cast<int64_t>(std::thread::hardware_concurrency());
+  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(8, cores / 2));
+  return static_cast<int>(std::min(by_size, cap));
+}
+
+// Waits until the device has read pinned slot s (its last copy is done).
+arc_status release_slot(arc_ctx* c, int s) {
   if (c->V_pending[s]) {
     ARC_HIP(hipEventSynchronize(c->V_done[s]), "hipEventSynchronize(projection)");
     c->V_pending[s] = false;
   }
-  if (c->use_override) {
-    std::memcpy(c->V_pinned[s], c->V_override.data(), c->V_override.size() * sizeof(float));
-  } else {
-    for (int64_t w : c->widths)
-      arc::generate_projection(c->seed, t, w, c->r, c->V_pinned[s] + c->v_off[w]);
+  return ARC_OK;
+}
+
+// Pinned staging + async copy of this step's projections.  After the copy
+// is queued, the pool starts on V_{t+1} in the other slot, so that a caller
+// stepping t, t+1, ... finds the next projection ready; any other t is
+// generated on the spot.
+arc_status upload_projection(arc_ctx* c, int64_t t) {
+  const int s = c->V_slot;
+  c->V_slot ^= 1;
+  c->V_pool->wait();
+  const bool ready = !c->use_override && c->V_prefetch_t == t;
+  c->V_prefetch_t = -1;
+  arc_status st;
+  if (!ready) {
+    if ((st = release_slot(c, s))) return st;
+    if (c->use_override) {
+      std::memcpy(c->V_pinned[s], c->V_override.data(), c->V_override.size() * sizeof(float));
+    } else {
+      c->V_pool->start(c->seed, t, c->r, &c->V_blocks, c->V_pinned[s]);
+      c->V_pool->wait();
+    }
   }
   ARC_HIP(hipMemcpyAsync(c->V_dev, c->V_pinned[s], static_cast<size_t>(c->v_floats) * sizeof(float),
                          hipMemcpyHostToDevice, c->stream),
           "hipMemcpyAsync(projection)");
   ARC_HIP(hipEventRecord(c->V_done[s], c->stream), "hipEventRecord(projection)");
   c->V_pending[s] = true;
+  if (!c->use_override && t < INT64_MAX) {
+    if ((st = release_slot(c, s ^ 1))) return st;
+    c->V_pool->start(c->seed, t + 1, c->r, &c->V_blocks, c->V_pinned[s ^ 1]);
+    c->V_prefetch_t = t + 1;
+  }
   return ARC_OK;
 }
 
@@ -596,6 +633,14 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
     if (e != hipSuccess) {
       c->V_done[s] = nullptr;
       return bail(fail_hip(e, "hipEventCreate"));
+    }
+  }
+  if (c->compressor == ARC_COMP_ARC) {
+    for (int64_t w : c->widths) c->V_blocks.push_back({w, c->v_off[w]});
+    try {
+      c->V_pool.reset(new arc::ProjectionPool(projection_threads(c->v_floats)));
+    } catch (const std::exception&) {
+      return bail(fail(ARC_ERR_NOMEM, "cannot start the projection threads"));
     }
   }
   // Constant tables, and zeroed radix scratch (kept zero between uses by the

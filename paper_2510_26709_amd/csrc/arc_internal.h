@@ -1,6 +1,11 @@
 // Internal declarations shared by the libarctopk host code and its kernels.
 #pragma once
 
+#include <condition_variable>
+#include <mutex>
+#include <thread>
+#include <vector>
+
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -203,5 +208,45 @@ hipError_t launch_optimizer(bool vec, const OptimizerArgs& o, const float* G, fl
 // V_t (n x r, row-major) for the shared seed and step t.
 void generate_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
                          float* V);
+// Rows [j0, j1) of the same V_t, written at V[j*r + k].
+void generate_projection_rows(uint64_t seed, int64_t t, int64_t n, int32_t r, int64_t j0,
+                              int64_t j1, float* V);
+
+// One width's V_t inside a staging buffer: `width` rows of r floats at
+// float offset `offset`.
+struct ProjectionBlock {
+  int64_t width;
+  int64_t offset;
+};
+
+// Host threads that fill a staging buffer with every width's V_t, so that
+// one step's projection can be generated while the device runs the previous
+// step.  start() returns at once (after any job still running has ended);
+// wait() returns when the last started job is complete.  The blocks and the
+// destination must stay valid until then.  One caller at a time.
+class ProjectionPool {
+ public:
+  explicit ProjectionPool(int threads);
+  ~ProjectionPool();
+  ProjectionPool(const ProjectionPool&) = delete;
+  ProjectionPool& operator=(const ProjectionPool&) = delete;
+  void start(uint64_t seed, int64_t t, int32_t r, const std::vector<ProjectionBlock>* blocks,
+             float* dst);
+  void wait();
+
+ private:
+  void run(int id);
+  std::vector<std::thread> threads_;
+  std::mutex mu_;
+  std::condition_variable cv_job_, cv_done_;
+  uint64_t job_ = 0;
+  int remaining_ = 0;
+  bool quit_ = false;
+  uint64_t seed_ = 0;
+  int64_t t_ = 0, total_rows_ = 0;
+  int32_t r_ = 0;
+  const std::vector<ProjectionBlock>* blocks_ = nullptr;
+  float* dst_ = nullptr;
+};
 
 }  // namespace arc

@@ -10,6 +10,9 @@
 // fully determined by (seed, t, n, r) and is identical on every node.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
+#include <thread>
+#include <vector>
 
 #include "arc_internal.h"
 
@@ -36,13 +39,13 @@ struct SplitMix64 {
 
 }  // namespace
 
-void generate_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
-                         float* V) {
+void generate_projection_rows(uint64_t seed, int64_t t, int64_t n, int32_t r, int64_t j0,
+                              int64_t j1, float* V) {
   constexpr double kTwoPi = 6.283185307179586476925286766559;
   constexpr double kTwoToMinus53 = 1.0 / 9007199254740992.0;
   const uint64_t un = static_cast<uint64_t>(n), ur = static_cast<uint64_t>(r);
   const uint64_t row0 = static_cast<uint64_t>(t) * un;
-  for (uint64_t j = 0; j < un; ++j) {
+  for (uint64_t j = static_cast<uint64_t>(j0); j < static_cast<uint64_t>(j1); ++j) {
     for (uint64_t k = 0; k < ur; ++k) {
       const uint64_t c = (row0 + j) * ur + k;
       SplitMix64 gen(seed, 2 * c);
@@ -54,6 +57,78 @@ void generate_projection(uint64_t seed, int64_t t, int64_t n, int32_t r,
       const double z = radius * std::cos(kTwoPi * u2);
       V[j * ur + k] = static_cast<float>(z);
     }
+  }
+}
+
+void generate_projection(uint64_t seed, int64_t t, int64_t n, int32_t r, float* V) {
+  generate_projection_rows(seed, t, n, r, 0, n, V);
+}
+
+// ---------------------------------------------------------------------------
+// ProjectionPool: the rows of every width's V_t split evenly over a few
+// threads.  Each entry is a pure function of (seed, t, j, k), so the split
+// changes no value.
+// ---------------------------------------------------------------------------
+ProjectionPool::ProjectionPool(int threads) {
+  if (threads < 1) threads = 1;
+  for (int i = 0; i < threads; ++i) threads_.emplace_back([this, i] { run(i); });
+}
+
+ProjectionPool::~ProjectionPool() {
+  {
+    std::lock_guard<std::mutex> lk(mu_);
+    quit_ = true;
+  }
+  cv_job_.notify_all();
+  for (std::thread& th : threads_) th.join();
+}
+
+void ProjectionPool::start(uint64_t seed, int64_t t, int32_t r,
+                           const std::vector<ProjectionBlock>* blocks, float* dst) {
+  wait();
+  std::lock_guard<std::mutex> lk(mu_);
+  seed_ = seed;
+  t_ = t;
+  r_ = r;
+  blocks_ = blocks;
+  dst_ = dst;
+  total_rows_ = 0;
+  for (const ProjectionBlock& b : *blocks) total_rows_ += b.width;
+  remaining_ = static_cast<int>(threads_.size());
+  ++job_;
+  cv_job_.notify_all();
+}
+
+void ProjectionPool::wait() {
+  std::unique_lock<std::mutex> lk(mu_);
+  cv_done_.wait(lk, [this] { return remaining_ == 0; });
+}
+
+void ProjectionPool::run(int id) {
+  uint64_t seen = 0;
+  const int nthreads = static_cast<int>(threads_.size());
+  for (;;) {
+    std::unique_lock<std::mutex> lk(mu_);
+    cv_job_.wait(lk, [&] { return quit_ || job_ != seen; });
+    if (quit_) return;
+    seen = job_;
+    const uint64_t seed = seed_;
+    const int64_t t = t_, total = total_rows_;
+    const int32_t r = r_;
+    const std::vector<ProjectionBlock>& blocks = *blocks_;
+    float* dst = dst_;
+    lk.unlock();
+    // This thread's share [lo, hi) of the rows of all widths, in block order.
+    const int64_t lo = total * id / nthreads, hi = total * (id + 1) / nthreads;
+    int64_t first = 0;
+    for (const ProjectionBlock& b : blocks) {
+      const int64_t j0 = lo > first ? lo - first : 0;
+      const int64_t j1 = hi - first < b.width ? hi - first : b.width;
+      if (j0 < j1) generate_projection_rows(seed, t, b.width, r, j0, j1, dst + b.offset);
+      first += b.width;
+    }
+    lk.lock();
+    if (--remaining_ == 0) cv_done_.notify_all();
   }
 }
 

@@ -69,8 +69,9 @@ def device_buffer(shape, dtype, dev, misalign_floats: int = 0) -> torch.Tensor:
 
 def run_case(*, d, N, n=0, r=4, K=0, eta=0.1, seed=7, grad_dtype="f32", buckets=None,
              tensors=None, steps=2, grad_fn=None, data_seed=11, family=0, V=None, misalign=0,
-             check_S=False, bit_exact=True, dev="cuda:0", label="case"):
-    """Run `steps` steps of libarctopk and of the oracle from h = g = 0.
+             check_S=False, bit_exact=True, dev="cuda:0", label="case", ts=None):
+    """Run `steps` steps of libarctopk and of the oracle from h = g = 0
+    (step numbers 0, 1, ..., or the sequence ts).
     tensors = [(rows, cols, K), ...] selects the per-tensor mode."""
     dev = torch.device(dev)
     gen = None
@@ -88,7 +89,7 @@ def run_case(*, d, N, n=0, r=4, K=0, eta=0.1, seed=7, grad_dtype="f32", buckets=
         g = device_buffer((N, d), torch.float32, dev, misalign)
         h_o = np.zeros((N, d), F32)
         g_o = np.zeros((N, d), F32)
-        for t in range(steps):
+        for t in (range(steps) if ts is None else ts):
             grad_np = grad_fn(t)
             grad = to_device_grad(grad_np, dev)
             if misalign:

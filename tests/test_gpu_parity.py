@@ -108,6 +108,18 @@ def test_describe_names_the_kernel_path():
         comp.close()
 
 
+def test_parity_steps_out_of_order():
+    # The library generates step t+1's projection while step t runs; a caller
+    # that skips, repeats or goes back in t gets V_t generated on the spot.
+    ts = [0, 1, 2, 7, 8, 3, 3, 0, 1]
+    run_case(label="out_of_order_single", d=256 * 300 + 40, N=3, n=256, r=4, K=9, ts=ts)
+    run_case(label="out_of_order_tensors", d=sum(a * b for a, b, _ in TENSORS_3W), N=4, r=4,
+             tensors=TENSORS_3W, ts=ts)
+
+
+TENSORS_3W = [(300, 64, 5), (40, 1000, 3), (129, 256, 4), (1, 2048, 1)]
+
+
 def test_parity_misaligned_pointers_take_the_general_path():
     log("[parity] misaligned")
     run_case(label="misaligned", d=256 * 120, N=3, n=256, r=4, K=11, steps=2, misalign=1)
