@@ -66,17 +66,21 @@ bool vector_r(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8; }
 // Rows per group of the vectorised sketch kernels for a view of width cols,
 // or 0 when the width needs the general kernel (not a multiple of 4, or a
 // group too large for 32-bit byte offsets).  Fewer rows per group give more,
-// shorter waves (the chunk widens instead): the first size whose chunk
-// divides the width, else the one with the widest chunk that fits in a row
-// (each row's last chunk is then partial).
-constexpr int32_t kGroupSizes[] = {16, 32, 64};
+// shorter waves whose rows are read in longer runs (the chunk widens
+// instead): the first size whose chunk divides the width, else the one with
+// the widest chunk that fits in a row (each row's last chunk is then
+// partial).  Measured on one MI355X against a 16-row minimum: ResNet-18
+// 0.38 -> 0.35 ms, per-tensor ResNet-18 0.54 -> 0.51 ms, GPT-2 small
+// 3.06 -> 3.00 ms (per tensor 3.23 -> 3.17), TinyLlama 11.87 -> 11.60 ms
+// (per tensor 12.02 -> 11.70).
+constexpr int32_t kGroupSizes[] = {8, 16, 32, 64};
 int32_t vector_group_rows(int64_t cols) {
   if (cols > (int64_t{1} << 22) || cols % 4 != 0) return 0;
   for (int32_t gr : kGroupSizes)
     if (cols % arc::vector_chunk_cols(gr) == 0) return gr;
   for (int32_t gr : kGroupSizes)
     if (cols >= arc::vector_chunk_cols(gr)) return gr;
-  return kGroupSizes[2];
+  return 64;
 }
 
 }  // namespace
@@ -310,31 +314,6 @@ void add_groups(int64_t elem_off, int64_t row0, int64_t rows, int64_t cols, int6
   }
 }
 
-// Order of one launch's row groups when their widths differ.  A wave's time
-// grows with the number of chunks in its rows, not with its row count, so
-// groups are sorted by descending chunk count (longest first), then dealt
-// round-robin over the 8 XCDs: the kernels' block remap gives XCD x table
-// entries [x*per, (x+1)*per), which hold sorted groups x, x+8, x+16, ...
-void balance_for_xcds(std::vector<arc::RowGroup>* groups, int32_t group_rows) {
-  const int64_t chunk = arc::vector_chunk_cols(group_rows);
-  std::vector<arc::RowGroup> sorted = *groups;
-  std::stable_sort(sorted.begin(), sorted.end(),
-                   [&](const arc::RowGroup& x, const arc::RowGroup& y) {
-                     return (x.cols + chunk - 1) / chunk > (y.cols + chunk - 1) / chunk;
-                   });
-  constexpr int64_t kXcds = 8;
-  const int64_t total = static_cast<int64_t>(sorted.size()), per = total / kXcds;
-  for (int64_t x = 0; x < kXcds; ++x)
-    for (int64_t j = 0; j < per; ++j) (*groups)[x * per + j] = sorted[j * kXcds + x];
-  for (int64_t b = per * kXcds; b < total; ++b) (*groups)[b] = sorted[b];
-}
-
-// Launches of fewer row groups than this (64 per compute unit) are balanced
-// over the XCDs; larger ones keep the tensors' row order, whose contiguous
-// ranges per XCD stream faster.  Measured on per-tensor layouts: ResNet-18
-// (about 400 groups) 1.00 -> 0.89 ms and GPT-2 small (7,200) 3.36 -> 3.25 ms
-// with balancing; TinyLlama (29,000) 11.87 ms without, 12.15 ms with it.
-constexpr size_t kBalanceBelowGroups = 64 * 256;
 
 // Selection buckets of one node's view (begin[0..nb], want[0..nb)).  Top-K
 // selects for every node separately over the N*m norms: node i's copies of
@@ -455,8 +434,6 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
   c->payload = nodes * c->payload_node;
   c->groups.clear();
   for (int sz = 0; sz < 4; ++sz) {
-    if (c->tensor_mode && lists.vec[sz].size() < kBalanceBelowGroups)
-      balance_for_xcds(&lists.vec[sz], 64 >> sz);
     c->vec_count[sz] = static_cast<int64_t>(lists.vec[sz].size());
     c->groups.insert(c->groups.end(), lists.vec[sz].begin(), lists.vec[sz].end());
   }
@@ -778,11 +755,15 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
                                        c->a, false, c->stream),
             "sketch launch (general rows)");
     if ((st = record(c, slot, 2))) return st;
-    // Stage 1: worker sum + importance of the rows the fused kernel did not do.
-    const int64_t done = fused ? nvec : 0;
-    ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + done,
-                                          ngroups - done, c->m, c->N, c->r, c->stream),
-            "reduce launch");
+    // Stage 1: worker sum + importance of the rows the fused kernel did not
+    // do: the general groups' rows, or every row.
+    if (fused)
+      ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + nvec,
+                                            ngroups - nvec, c->m, c->N, c->r, c->stream),
+              "reduce launch");
+    else
+      ARC_HIP(arc::launch_reduce_rows(c->S_dev, c->sigma_dev, c->m, c->N, c->r, c->stream),
+              "reduce launch");
     if ((st = record(c, slot, 3))) return st;
     // Stage 2: per-bucket top-K.
     ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");

@@ -162,6 +162,9 @@ hipError_t launch_reduce_importance(const float* S, float* sigma,
                                     const RowGroup* groups, int64_t ngroups,
                                     int64_t m, int32_t N, int32_t r,
                                     hipStream_t stream);
+// The same for every row 0 .. m-1 (one thread per row).
+hipError_t launch_reduce_rows(const float* S, float* sigma, int64_t m, int32_t N, int32_t r,
+                              hipStream_t stream);
 
 // Per-bucket arg-top-K of sigma into out_idx (ascending per bucket).
 hipError_t launch_select(const float* sigma, const SelectWorkspace& ws,

@@ -304,15 +304,10 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   }
 }
 
-// Worker sum and importance from S for the rows of groups[0 .. ngroups); one
-// 64-thread block per group, one thread per row.
-__global__ void __launch_bounds__(kWave)
-reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
-                         const RowGroup* __restrict__ groups, int64_t m, int32_t N,
-                         int32_t r) {
-  const RowGroup grp = groups[blockIdx.x];
-  if ((int32_t)threadIdx.x >= grp.rows) return;
-  const int64_t p = grp.row0 + threadIdx.x;
+// Worker sum P = S^(0) + S^(1) + ... (ascending worker order) and importance
+// sum_k P_k^2 (fma chain in ascending k) of row p.
+__device__ __forceinline__ void reduce_row(const float* __restrict__ S, float* __restrict__ sigma,
+                                           int64_t p, int64_t m, int32_t N, int32_t r) {
   float acc = 0.0f;
   if (r == 4) {
     float4 P = *reinterpret_cast<const float4*>(S + p * 4);
@@ -335,6 +330,24 @@ reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
     }
   }
   sigma[p] = acc;
+}
+
+// For the rows of groups[0 .. ngroups): one 64-thread block per group, one
+// thread per row.
+__global__ void __launch_bounds__(kWave)
+reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
+                         const RowGroup* __restrict__ groups, int64_t m, int32_t N,
+                         int32_t r) {
+  const RowGroup grp = groups[blockIdx.x];
+  if ((int32_t)threadIdx.x < grp.rows) reduce_row(S, sigma, grp.row0 + threadIdx.x, m, N, r);
+}
+
+// For every row: one thread per row.
+__global__ void __launch_bounds__(256)
+reduce_rows_kernel(const float* __restrict__ S, float* __restrict__ sigma, int64_t m, int32_t N,
+                   int32_t r) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < m) reduce_row(S, sigma, p, m, N, r);
 }
 
 }  // namespace
@@ -449,6 +462,14 @@ hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_b
       return hipErrorInvalidValue;
   }
 #undef ARC_NORM_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_rows(const float* S, float* sigma, int64_t m, int32_t N, int32_t r,
+                              hipStream_t stream) {
+  if (m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_rows_kernel, dim3(blocks_for(m, 256)), dim3(256), 0, stream, S,
+                     sigma, m, N, r);
   return hipGetLastError();
 }
 

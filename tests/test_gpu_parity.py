@@ -56,7 +56,8 @@ CASES = [
     ("generic_wide_ragged", dict(d=1000 * 70 + 999, N=3, n=1000, r=4, K=5, steps=2)),
     ("generic_many_workers", dict(d=50 * 257, N=11, n=50, r=4, K=20, steps=2)),
     # fused kernel (N <= 3) and per-worker kernel (N >= 4) for every r and
-    # row-group size (16 rows for n % 128 == 0, 32 for n % 64, 64 otherwise)
+    # row-group size (8 rows for n % 256 == 0, 16 for n % 128, 32 for n % 64,
+    # 64 otherwise)
     ("fused_r2_g64", dict(d=96 * 513, N=2, n=96, r=2, K=7, steps=2)),
     ("fused_g32_bf16", dict(d=192 * 400, N=3, n=192, r=4, K=9, steps=2, grad_dtype="bf16",
                             family=1)),
@@ -64,6 +65,10 @@ CASES = [
     ("per_worker_r8_g64", dict(d=32 * 4097, N=4, n=32, r=8, K=100, steps=2)),
     ("per_worker_r1_bf16", dict(d=128 * 777, N=5, n=128, r=1, K=30, steps=2, grad_dtype="bf16",
                                 family=1)),
+    ("fused_g8_r8_bf16", dict(d=256 * 700 + 36, N=3, n=256, r=8, K=9, steps=2, grad_dtype="bf16",
+                              family=1)),
+    ("per_worker_g8_r2", dict(d=512 * 400, N=6, n=512, r=2, K=9, steps=2)),
+    ("fused_g16_r4", dict(d=128 * 900, N=2, n=128, r=4, K=9, steps=2)),
     # widths that are multiples of 4 but not of the chunk: every row's last
     # chunk is partial (32 + 4, 64 + 36, 7 x 128 + 104 columns), and the
     # ragged tail row is a one-row vector group as wide as its values
