@@ -175,6 +175,11 @@ def model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb, t0, steps=5,
     (arc_model_step), timed on the library's stream after the main timed
     region.  Reported beside the compressor-only value."""
     dev = h.device
+    need = 4 * 4 * w.d + (1 << 30)  # G, x and Adam's m, v, plus slack
+    free, _ = torch.cuda.mem_get_info(dev)
+    if free < need:
+        return {"skipped": f"needs {need / 1e9:.1f} GB of free device memory, "
+                           f"{free / 1e9:.1f} GB free beside the compressor's buffers"}
     G, x, m, v = (torch.zeros(w.d, dtype=torch.float32, device=dev) for _ in range(4))
     mc = arc.make_model_config("adam", lr=1e-3, weight_decay=5e-4)
     for k in range(warmup):
@@ -195,9 +200,9 @@ def model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb, t0, steps=5,
             "adam_update_bytes": opt_bytes}
 
 
-def copy_calibration(torch, gib, reps):
-    """Plain device-to-device copy of a known size: every launch reads and
-    writes `gib` GiB exactly once."""
+def time_copy(torch, gib, reps):
+    """Plain device-to-device copy of a known size (every launch reads and
+    writes `gib` GiB once): (bytes copied, mean ms per copy)."""
     nbytes = int(gib * 2**30) // 16 * 16
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
@@ -210,6 +215,13 @@ def copy_calibration(torch, gib, reps):
     end.record()
     end.synchronize()
     ms = start.elapsed_time(end) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return nbytes, ms
+
+
+def copy_calibration(torch, gib, reps):
+    nbytes, ms = time_copy(torch, gib, reps)
     print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps,
                       "ms_per_copy": ms, "GBps_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}),
           flush=True)
@@ -315,6 +327,11 @@ def main():
     value = w.N * w.d / (ms_per_step * 1e-3)
     step_gbps = byt["step"] / (ms_per_step * 1e-3) / 1e9
 
+    # An empirical ceiling beside the vendor peak: a plain 2 GiB device copy
+    # (torch's copy_, the runtime's copy kernel), timed in the same process.
+    nbytes, copy_ms = time_copy(torch, 2, 10)
+    copy_gbps = 2 * nbytes / (copy_ms * 1e-3) / 1e9
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
@@ -364,6 +381,9 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": byt["sketch_kernel"],
             "mean_launch_ms": sk_ms,
+            "copy_ceiling": {"GBps": copy_gbps, "bytes_read_plus_written": 2 * nbytes,
+                             "kernel": "device-to-device copy (torch copy_)",
+                             "achieved_over_copy": achieved / copy_gbps},
         },
         "cpu_baseline": cpu,
         "ef21m_iteration": model,
