@@ -163,9 +163,11 @@ struct arc_ctx {
     ws.nblk = static_cast<int32_t>(blocks.size());
     ws.any_radix = 0;
     ws.any_output = 0;
+    ws.small = 1;
     for (const auto& b : buckets) {
       ws.any_radix |= b.mode == arc::kSelectRadix;
       ws.any_output |= b.mode != arc::kSelectNone;
+      ws.small &= b.hi - b.lo <= arc::kSmallBucketRows;
     }
     return ws;
   }

@@ -90,7 +90,16 @@ struct SelectWorkspace {
   int32_t nb, nblk;
   int32_t any_radix;   // some bucket needs the radix passes
   int32_t any_output;  // some bucket selects at least one row
+  int32_t small;       // every bucket has at most kSmallBucketRows rows
 };
+
+// Buckets of at most this many rows are selected by one workgroup each, in
+// one launch for the whole step (no global histograms or block counts).
+// Larger buckets gain from spreading the histogram atomics over several
+// compute units: at 22,832 rows one workgroup took as long as the five
+// multi-block launches.
+constexpr int kSmallSelectThreads = 1024;
+constexpr int64_t kSmallBucketRows = 8 * kSmallSelectThreads;
 
 // ---- launchers; each returns hipGetLastError() ----
 

@@ -21,6 +21,10 @@
 //              step.
 // No kernel waits on another block: there are no grid-wide counters, and the
 // result does not depend on scheduling.
+//
+// When every bucket has at most kSmallBucketRows rows, one launch of
+// select_small_kernel does all of this instead, one 1024-thread workgroup per
+// bucket, with the histograms, the radix state and the counts in LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -192,9 +196,10 @@ select_count_kernel(const float* __restrict__ sigma, SelectWorkspace ws) {
   }
 }
 
-// Exclusive prefix sum over the block (blockDim.x == kSelectThreads).
+// Exclusive prefix sum over the block (blockDim.x == THREADS).
+template <int THREADS = kSelectThreads>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v) {
-  __shared__ uint32_t wsum[kSelectThreads / kWave];
+  __shared__ uint32_t wsum[THREADS / kWave];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const uint32_t incl = wave_inclusive_scan(v);
@@ -202,7 +207,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v) {
   __syncthreads();
   uint32_t before = 0;
 #pragma unroll
-  for (int w = 0; w < kSelectThreads / kWave; ++w)
+  for (int w = 0; w < THREADS / kWave; ++w)
     if (w < wave) before += wsum[w];
   __syncthreads();
   return before + incl - v;
@@ -301,10 +306,102 @@ select_write_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
   }
 }
 
+// Histogram of digit PASS of the bucket's keys that match st, into the
+// block's LDS histogram (cleared here), then the digit fixed from it.
+template <int PASS>
+__device__ BucketState small_pass(const float* __restrict__ sigma, const BucketDesc& bk,
+                                  BucketState st, uint32_t* lhist, BucketState* sh) {
+  using D = RadixDigit<PASS>;
+  for (int b = threadIdx.x; b < D::kBins; b += kSmallSelectThreads) lhist[b] = 0u;
+  __syncthreads();
+  for (int64_t base = bk.lo; base < bk.hi; base += kSmallSelectThreads * kKeysPerBatch) {
+    uint32_t keys[kKeysPerBatch];
+    bool valid[kKeysPerBatch];
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u) {
+      const int64_t p = base + u * kSmallSelectThreads + threadIdx.x;
+      valid[u] = p < bk.hi;
+      keys[u] = valid[u] ? __float_as_uint(sigma[p]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kKeysPerBatch; ++u)
+      if (valid[u] && (keys[u] & st.mask) == st.prefix)
+        atomicAdd(&lhist[(keys[u] >> D::kShift) & D::kMask], 1u);
+  }
+  __syncthreads();
+  if (threadIdx.x < kWave) {
+    const BucketState next = fix_digit<PASS>(lhist, st);
+    if (threadIdx.x == 0) *sh = next;
+  }
+  __syncthreads();
+  return *sh;
+}
+
+// One workgroup per bucket: the three radix passes, then the write of the
+// kept rows in ascending order, ties to the lower row (as the multi-block
+// kernels, with the block's threads in the roles of the blocks).
+__global__ void __launch_bounds__(kSmallSelectThreads)
+select_small_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
+                    int32_t* __restrict__ out_idx) {
+  __shared__ uint32_t lhist[kRadixBins];
+  __shared__ BucketState sh;
+  const BucketDesc bk = ws.buckets[blockIdx.x];
+  if (bk.mode == kSelectNone) return;  // whole block
+  if (bk.mode == kSelectAll) {
+    for (int64_t p = bk.lo + threadIdx.x; p < bk.hi; p += kSmallSelectThreads)
+      out_idx[bk.out_off + (p - bk.lo)] = (int32_t)p;
+    return;
+  }
+  BucketState st;
+  st.prefix = 0u;
+  st.mask = 0u;
+  st.kleft = bk.k;
+  st = small_pass<0>(sigma, bk, st, lhist, &sh);
+  st = small_pass<1>(sigma, bk, st, lhist, &sh);
+  st = small_pass<2>(sigma, bk, st, lhist, &sh);
+  const uint32_t T = st.prefix;
+  const uint64_t kleft = (uint64_t)st.kleft;
+  // Thread t owns rows [r0, r1), contiguous, so thread order is row order.
+  const int64_t rows = bk.hi - bk.lo;
+  const int64_t rpt = (rows + kSmallSelectThreads - 1) / kSmallSelectThreads;
+  const int64_t r0 = bk.lo + (int64_t)threadIdx.x * rpt;
+  const int64_t r1 = r0 + rpt < bk.hi ? r0 + rpt : bk.hi;
+  uint32_t n_eq = 0, n_gt = 0;
+  for (int64_t p = r0; p < r1; ++p) {
+    const uint32_t key = __float_as_uint(sigma[p]);
+    n_gt += key > T;
+    n_eq += key == T;
+  }
+  const uint64_t eq_rank0 = block_exclusive_scan<kSmallSelectThreads>(n_eq);
+  const uint64_t ties_kept =
+      eq_rank0 >= kleft ? 0 : ((kleft - eq_rank0) < n_eq ? (kleft - eq_rank0) : n_eq);
+  int64_t pos = bk.out_off +
+                block_exclusive_scan<kSmallSelectThreads>(n_gt + (uint32_t)ties_kept);
+  const int64_t end = bk.out_off + bk.k;
+  uint64_t rank = eq_rank0;
+  for (int64_t p = r0; p < r1; ++p) {
+    const uint32_t key = __float_as_uint(sigma[p]);
+    bool sel = key > T;
+    if (key == T) {
+      sel = rank < kleft;
+      ++rank;
+    }
+    // pos stays below the bucket's end by construction; the bound keeps a
+    // broken invariant from writing outside out_idx.
+    if (sel && pos < end) out_idx[pos++] = (int32_t)p;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_select(const float* sigma, const SelectWorkspace& ws,
                          int32_t* out_idx, hipStream_t stream) {
+  if (ws.small) {
+    if (ws.any_output)
+      hipLaunchKernelGGL(select_small_kernel, dim3((unsigned)ws.nb), dim3(kSmallSelectThreads), 0,
+                         stream, sigma, ws, out_idx);
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)ws.nblk), block(kSelectThreads);
   if (ws.any_radix) {
     hipLaunchKernelGGL(radix_pass_kernel<0>, grid, block, 0, stream, sigma, ws);

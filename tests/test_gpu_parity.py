@@ -140,27 +140,31 @@ def test_parity_buckets():
     run_case(label="buckets", d=d, N=3, n=n, r=4, buckets=(begin, ks), steps=3)
 
 
-def test_parity_zero_residual_ties_take_lowest_rows():
-    d, N, n = 256 * 400, 2, 256
+# Selections over at most 8192 rows per bucket take the one-workgroup path,
+# larger ones the multi-block radix kernels: both sizes for the tie cases.
+@pytest.mark.parametrize("rows", [400, 40_000])
+def test_parity_zero_residual_ties_take_lowest_rows(rows):
+    d, N, n = 32 * rows, 2, 32
     zero = np.zeros((N, d), F32)
-    log("[parity] zero residual")
-    run_case(label="zeros", d=d, N=N, n=n, K=13, steps=2, grad_fn=lambda t: zero)
+    log(f"[parity] zero residual, {rows} rows")
+    run_case(label=f"zeros_{rows}", d=d, N=N, n=n, K=13, steps=2, grad_fn=lambda t: zero)
 
 
-def test_parity_crafted_ties():
+@pytest.mark.parametrize("rows,K", [(5000, 1234), (70_000, 17_321)])
+def test_parity_crafted_ties(rows, K):
     # V = ones (r = 1): Sigma_p = (sum over workers and row of Delta)^2, built
     # from small integers so that many rows tie exactly at the threshold.
-    d, N, n = 32 * 5000, 2, 32
+    d, N, n = 32 * rows, 2, 32
     rng = np.random.default_rng(5)
-    vals = rng.integers(0, 4, size=(5000,)).astype(F32)  # row sums in {0..3}
+    vals = rng.integers(0, 4, size=(rows,)).astype(F32)  # row sums in {0..3}
 
     def grad(t):
         g = np.zeros((N, d), F32)
         g[0, ::n] = vals  # first column of each row for worker 0
         return g
 
-    log("[parity] crafted ties")
-    run_case(label="ties", d=d, N=N, n=n, r=1, K=1234, eta=1.0, steps=1, grad_fn=grad,
+    log(f"[parity] crafted ties, {rows} rows")
+    run_case(label=f"ties_{rows}", d=d, N=N, n=n, r=1, K=K, eta=1.0, steps=1, grad_fn=grad,
              V=np.ones((n, 1), F32))
 
 
