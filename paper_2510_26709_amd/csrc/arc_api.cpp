@@ -107,11 +107,16 @@ struct arc_ctx {
   std::vector<arc::RowGroup> groups;
   int64_t nvec_groups = 0;
   std::array<int64_t, 4> vec_count{};  // groups of 64, 32, 16 and 8 rows
+  std::array<int64_t, 5> stage_elems{};  // coordinates per launch: those sizes, general
   // per-tensor gather
   std::vector<arc::GatherBucket> gather;
   int64_t gather_work = 0;
   // device
   hipStream_t stream = nullptr;
+  // second stream for the smaller launches of the streaming stage, forked
+  // from and joined back into `stream` (only when there are several)
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   int device = 0;
   size_t max_lds_per_block = 0;
   float* V_dev = nullptr;
@@ -175,6 +180,12 @@ struct arc_ctx {
   void release() {
     V_pool.reset();  // joins the threads before their buffers go
     (void)hipStreamSynchronize(stream);
+    if (side) {
+      (void)hipStreamSynchronize(side);
+      (void)hipStreamDestroy(side);
+    }
+    for (hipEvent_t e : {fork_ev, join_ev})
+      if (e) (void)hipEventDestroy(e);
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
                     static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
                     static_cast<void*>(sel_dev),
@@ -437,10 +448,14 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
   c->groups.clear();
   for (int sz = 0; sz < 4; ++sz) {
     c->vec_count[sz] = static_cast<int64_t>(lists.vec[sz].size());
+    for (const arc::RowGroup& grp : lists.vec[sz])
+      c->stage_elems[sz] += (grp.rows - 1) * static_cast<int64_t>(grp.cols) + grp.last_len;
     c->groups.insert(c->groups.end(), lists.vec[sz].begin(), lists.vec[sz].end());
   }
   c->nvec_groups = static_cast<int64_t>(c->groups.size());
   c->groups.insert(c->groups.end(), lists.general.begin(), lists.general.end());
+  for (const arc::RowGroup& grp : lists.general)
+    c->stage_elems[4] += (grp.rows - 1) * static_cast<int64_t>(grp.cols) + grp.last_len;
 }
 
 template <typename T>
@@ -622,6 +637,16 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
       return bail(fail(ARC_ERR_NOMEM, "cannot start the projection threads"));
     }
   }
+  {
+    int launches = c->stage_elems[4] > 0 ? 1 : 0;
+    for (int sz = 0; sz < 4; ++sz) launches += c->vec_count[sz] > 0;
+    if (launches > 1) {
+      e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork_ev, hipEventDisableTiming);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming);
+      if (e != hipSuccess) return bail(fail_hip(e, "hipStreamCreate(side)"));
+    }
+  }
   // Constant tables, and zeroed radix scratch (kept zero between uses by the
   // kernels themselves).
   e = upload(c->buckets_dev, c->buckets);
@@ -672,6 +697,73 @@ arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const 
   return ARC_OK;
 }
 
+// The streaming stage (S1-S3, plus S4 for the fused kernel; norm: Top-K's
+// row norms): one launch per row-group size present and one for the general
+// groups.  When there are several, the one over the most coordinates runs on
+// the caller's stream and the others on the second stream, forked after
+// everything queued before and joined before anything queued after, so that
+// they overlap it instead of following it.
+arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const float* g,
+                                  int64_t nvec, int64_t ngroups, bool fused, bool norm) {
+  int which[5], nl = 0, big = 0;
+  for (int sz = 0; sz < 4; ++sz)
+    if (nvec > 0 && c->vec_count[sz] > 0) which[nl++] = sz;
+  if (ngroups > nvec) which[nl++] = 4;
+  // With misaligned pointers every group is general: one launch.
+  const auto elems = [&](int w) {
+    if (w < 4) return c->stage_elems[w];
+    return nvec > 0 ? c->stage_elems[4] : c->m;  // m stands in for "all of them"
+  };
+  for (int l = 1; l < nl; ++l)
+    if (elems(which[l]) > elems(which[big])) big = l;
+  const bool fork = nl > 1 && c->side != nullptr;
+  if (fork) {
+    ARC_HIP(hipEventRecord(c->fork_ev, c->stream), "hipEventRecord(fork)");
+    ARC_HIP(hipStreamWaitEvent(c->side, c->fork_ev, 0), "hipStreamWaitEvent(fork)");
+  }
+  // The smaller launches go first, so that they start while the largest
+  // fills the rest of the device.
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int l = 0; l < nl; ++l) {
+      if ((l == big) != (pass == 1)) continue;
+      hipStream_t s = fork && l != big ? c->side : c->stream;
+      const int w = which[l];
+      if (w == 4) {
+        ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev,
+                                           c->groups_dev + nvec, ngroups - nvec, c->S_dev, c->d,
+                                           c->m, c->N, norm ? 1 : c->r, c->eta, c->a, norm, s),
+                norm ? "row norm launch (general rows)" : "sketch launch (general rows)");
+        continue;
+      }
+      int64_t first = 0;
+      for (int sz = 0; sz < w; ++sz) first += c->vec_count[sz];
+      const int32_t gr = 64 >> w;
+      const arc::RowGroup* grp = c->groups_dev + first;
+      if (norm) {
+        ARC_HIP(arc::launch_row_norms(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
+                                      c->vec_count[w], c->S_dev, c->d, c->m, c->N, c->eta, c->a,
+                                      s),
+                "row norm launch");
+      } else if (fused) {
+        ARC_HIP(arc::launch_sketch_fused(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
+                                         c->vec_count[w], c->S_dev, c->sigma_dev, c->d, c->m,
+                                         c->N, c->r, c->eta, c->a, s),
+                "fused sketch launch");
+      } else {
+        ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
+                                              c->vec_count[w], c->S_dev, c->d, c->m, c->N,
+                                              c->r, c->eta, c->a, s),
+                "sketch launch");
+      }
+    }
+  }
+  if (fork) {
+    ARC_HIP(hipEventRecord(c->join_ev, c->side), "hipEventRecord(join)");
+    ARC_HIP(hipStreamWaitEvent(c->stream, c->join_ev, 0), "hipStreamWaitEvent(join)");
+  }
+  return ARC_OK;
+}
+
 // The compressor step (arguments already checked); with a non-null G the
 // payload is also added into G at the selected coordinates.
 arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
@@ -710,15 +802,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
     if ((st = record(c, slot, 4))) return st;
   } else if (c->compressor == ARC_COMP_TOPK) {
     // Stage 0: Eq. (11a) with every node's squared row norms of Delta.
-    for (int sz = 0, first = 0; nvec > 0 && sz < 4; first += c->vec_count[sz], ++sz)
-      ARC_HIP(arc::launch_row_norms(64 >> sz, grad, c->grad_bf16, h, g, c->V_dev,
-                                    c->groups_dev + first, c->vec_count[sz], c->S_dev, c->d,
-                                    c->m, c->N, c->eta, c->a, c->stream),
-              "row norm launch");
-    ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
-                                       ngroups - nvec, c->S_dev, c->d, c->m, c->N, 1, c->eta,
-                                       c->a, true, c->stream),
-            "row norm launch (general rows)");
+    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, false, true))) return st;
     if ((st = record(c, slot, 2))) return st;
     if ((st = record(c, slot, 3))) return st;
     // Stage 2: every node's own top-K over its norms.
@@ -736,26 +820,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   } else {
     // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
     // the fused kernel also forms the worker sum and importance of its rows.
-    // One launch per group size present (64, 32, 16 rows).
-    for (int sz = 0, first = 0; nvec > 0 && sz < 4; first += c->vec_count[sz], ++sz) {
-      const int32_t gr = 64 >> sz;
-      const arc::RowGroup* grp = c->groups_dev + first;
-      if (fused) {
-        ARC_HIP(arc::launch_sketch_fused(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
-                                         c->vec_count[sz], c->S_dev, c->sigma_dev, c->d, c->m,
-                                         c->N, c->r, c->eta, c->a, c->stream),
-                "fused sketch launch");
-      } else {
-        ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
-                                              c->vec_count[sz], c->S_dev, c->d, c->m, c->N,
-                                              c->r, c->eta, c->a, c->stream),
-                "sketch launch");
-      }
-    }
-    ARC_HIP(arc::launch_sketch_general(grad, c->grad_bf16, h, g, c->V_dev, c->groups_dev + nvec,
-                                       ngroups - nvec, c->S_dev, c->d, c->m, c->N, c->r, c->eta,
-                                       c->a, false, c->stream),
-            "sketch launch (general rows)");
+    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, fused, false))) return st;
     if ((st = record(c, slot, 2))) return st;
     // Stage 1: worker sum + importance of the rows the fused kernel did not
     // do: the general groups' rows, or every row.
