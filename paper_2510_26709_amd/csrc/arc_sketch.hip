@@ -31,16 +31,33 @@ struct GroupShape {
 };
 constexpr int kTileF4 = 576;  // >= G * (512 / G + 1) for every G
 
+// (row, k) lanes: when G * R <= 64, lane l runs only the chain of row l % G
+// against column (l / G) % R of V, and the R results of a row are collected
+// from their lanes at the end.  Otherwise every lane runs all R chains of
+// row l % G.
+template <int R, int G, bool NORM>
+constexpr bool k_split() { return !NORM && G * R <= kWave; }
+
 // After its tile, a wave's LDS holds the projection rows of the current
 // chunk (CW x R binary32), so that the chains read V from LDS: wave-uniform
 // scalar loads of V would share the lgkm counter with the tile reads, and a
-// wait for one would be a wait for both.
+// wait for one would be a wait for both.  With (row, k) lanes the slice is
+// transposed, [k][column] with a pitch of CW + 4 floats (each lane reads its
+// column of V as float4s, and the R columns fall in distinct banks).
 template <int R, int G, bool NORM>
-constexpr int slice_f4() { return NORM ? 0 : GroupShape<G>::kChunkCols * R / 4; }
+constexpr int slice_src_f4() { return NORM ? 0 : GroupShape<G>::kChunkCols * R / 4; }
+template <int R, int G, bool NORM>
+constexpr int slice_f4() {
+  return k_split<R, G, NORM>() ? R * (GroupShape<G>::kChunkCols + 4) / 4
+                               : slice_src_f4<R, G, NORM>();
+}
 template <int R, int G, bool NORM>
 constexpr int wave_lds_f4() { return kTileF4 + slice_f4<R, G, NORM>(); }
-constexpr int kMaxWaveLdsF4 = kTileF4 + 512;  // largest slice: R = 8, G = 8
-constexpr uint32_t kDropOffset = 0x80000000u;  // beyond every buffer resource here
+constexpr int kMaxWaveLdsF4 = kTileF4 + 520;  // largest slice: R = 8, G = 8, transposed
+// Offset whose access the hardware drops: a group spans at most 2^30 bytes
+// (64 rows of at most 2^22 binary32 values), so 2^31, and the 2^30 it becomes
+// for the bf16 stream's halved offsets, lie beyond every resource here.
+constexpr uint32_t kDropOffset = 0x80000000u;
 
 // One wave's pass over the rows of one row group of worker i: loads the
 // grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
@@ -61,7 +78,8 @@ __device__ __forceinline__ void sketch_rows(
     const RowGroup& grp, int32_t i, float eta, float a, float4* tile,
     float (&s)[R]) {
   using Shape = GroupShape<G>;
-  constexpr int kSliceF4 = slice_f4<R, G, NORM>();
+  constexpr bool kSplit = k_split<R, G, NORM>();
+  constexpr int kSliceF4 = slice_src_f4<R, G, NORM>();  // float4 of V per chunk
   constexpr int kSliceRegs = (kSliceF4 + kWave - 1) / kWave;
   constexpr int kLPR = Shape::kLanesPerRow;
   constexpr int kRPL = Shape::kRowsPerLoad;
@@ -86,6 +104,7 @@ __device__ __forceinline__ void sketch_rows(
   for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * kRPL + sub) * n + quad * 4) * 4u;
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
+  float s_own = 0.0f;  // (row, k) lanes: this lane's chain
 
   const uint32_t nchunks = (n + kCW - 1) / kCW;
   // Columns of the last chunk: kCW unless the width is not a multiple of it.
@@ -182,7 +201,18 @@ __device__ __forceinline__ void sketch_rows(
       tile[(u * kRPL + sub) * kPitch + quad] = dl;
       off[u] += kCW * 4;
     }
-    if constexpr (kSliceF4 > 0) {
+    if constexpr (kSliceF4 > 0 && kSplit) {
+      float* vt = reinterpret_cast<float*>(vslice);
+#pragma unroll
+      for (int r4 = 0; r4 < kSliceRegs; ++r4) {
+        const int f = slice_at(r4, c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int idx = 4 * f + e;  // V[idx / R][idx % R] of the chunk
+          vt[(idx % R) * (kCW + 4) + idx / R] = vreg[4 * r4 + e];
+        }
+      }
+    } else if constexpr (kSliceF4 > 0) {
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
         vslice[slice_at(r4, c)] =
@@ -194,7 +224,23 @@ __device__ __forceinline__ void sketch_rows(
     wave_lds_fence();
     const float* Vc = reinterpret_cast<const float*>(vslice);
     const float4* my_row = tile + (lane & (G - 1)) * kPitch;
-    if (c + 1 < nchunks || tail == kCW) {
+    if constexpr (kSplit) {
+      const float* vk = Vc + ((lane / G) % R) * (kCW + 4);
+      if (c + 1 < nchunks || tail == kCW) {
+#pragma unroll
+        for (int q = 0; q < kLPR; ++q) {
+          const float4 dv = my_row[q];
+          const float4 v4 = *reinterpret_cast<const float4*>(vk + q * 4);
+          s_own = fmaf(dv.x, v4.x, s_own);
+          s_own = fmaf(dv.y, v4.y, s_own);
+          s_own = fmaf(dv.z, v4.z, s_own);
+          s_own = fmaf(dv.w, v4.w, s_own);
+        }
+      } else {
+        const float* rowf = reinterpret_cast<const float*>(my_row);
+        for (uint32_t j = 0; j < tail; ++j) s_own = fmaf(rowf[j], vk[j], s_own);
+      }
+    } else if (c + 1 < nchunks || tail == kCW) {
 #pragma unroll
       for (int q = 0; q < kLPR; ++q) {
         const float4 dv = my_row[q];
@@ -224,6 +270,11 @@ __device__ __forceinline__ void sketch_rows(
       }
     }
     wave_lds_fence();
+  }
+  if constexpr (kSplit) {
+    // Row l % G's R results, from lanes l % G + k * G.
+#pragma unroll
+    for (int k = 0; k < R; ++k) s[k] = __shfl(s_own, (lane & (G - 1)) + k * G, kWave);
   }
 }
 
