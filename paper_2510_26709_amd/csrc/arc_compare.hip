@@ -29,7 +29,7 @@ momentum_vec_kernel(const void* __restrict__ grad, float* __restrict__ h, int64_
   } else {
     x = stream_load(reinterpret_cast<const float4*>(static_cast<const float*>(grad) + e));
   }
-  float4 hv = *reinterpret_cast<const float4*>(h + e);
+  float4 hv = stream_load(reinterpret_cast<const float4*>(h + e));
   hv.x = fmaf(eta, x.x, a * hv.x);
   hv.y = fmaf(eta, x.y, a * hv.y);
   hv.z = fmaf(eta, x.z, a * hv.z);

@@ -43,8 +43,8 @@ dense_step_vec_kernel(const void* __restrict__ grad, float* __restrict__ h,
   for (int32_t i = 0; i < N; ++i) {
     const int64_t at = (int64_t)i * d + e;
     const float4 x = load_grad4<BF16>(grad, at);
-    float4 hv = *reinterpret_cast<const float4*>(h + at);
-    const float4 gv = *reinterpret_cast<const float4*>(g + at);
+    float4 hv = stream_load(reinterpret_cast<const float4*>(h + at));
+    const float4 gv = stream_load(reinterpret_cast<const float4*>(g + at));
     hv.x = fmaf(eta, x.x, a * hv.x);
     hv.y = fmaf(eta, x.y, a * hv.y);
     hv.z = fmaf(eta, x.z, a * hv.z);
@@ -62,12 +62,12 @@ dense_step_vec_kernel(const void* __restrict__ grad, float* __restrict__ h,
     stream_store(reinterpret_cast<float4*>(g + at),
                  make_float4(gv.x + dl.x, gv.y + dl.y, gv.z + dl.z, gv.w + dl.w));
   }
-  float4 Gv = *reinterpret_cast<const float4*>(G + e);
+  float4 Gv = stream_load(reinterpret_cast<const float4*>(G + e));
   Gv.x = Gv.x + acc.x;
   Gv.y = Gv.y + acc.y;
   Gv.z = Gv.z + acc.z;
   Gv.w = Gv.w + acc.w;
-  *reinterpret_cast<float4*>(G + e) = Gv;
+  stream_store(reinterpret_cast<float4*>(G + e), Gv);
 }
 
 __global__ void __launch_bounds__(256)
@@ -127,17 +127,17 @@ optimizer_vec_kernel(OptimizerArgs o, const float* __restrict__ G, float* __rest
   const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (e >= d) return;
   const float4 Gv = stream_load(reinterpret_cast<const float4*>(G + e));
-  float4 xv = *reinterpret_cast<const float4*>(x + e);
+  float4 xv = stream_load(reinterpret_cast<const float4*>(x + e));
   float4 mv = make_float4(0.f, 0.f, 0.f, 0.f), vv = mv;
-  if constexpr (KIND >= 1) mv = *reinterpret_cast<const float4*>(m + e);
-  if constexpr (KIND == 2) vv = *reinterpret_cast<const float4*>(v + e);
+  if constexpr (KIND >= 1) mv = stream_load(reinterpret_cast<const float4*>(m + e));
+  if constexpr (KIND == 2) vv = stream_load(reinterpret_cast<const float4*>(v + e));
   update_one<KIND>(o, Gv.x, xv.x, mv.x, vv.x);
   update_one<KIND>(o, Gv.y, xv.y, mv.y, vv.y);
   update_one<KIND>(o, Gv.z, xv.z, mv.z, vv.z);
   update_one<KIND>(o, Gv.w, xv.w, mv.w, vv.w);
-  *reinterpret_cast<float4*>(x + e) = xv;
-  if constexpr (KIND >= 1) *reinterpret_cast<float4*>(m + e) = mv;
-  if constexpr (KIND == 2) *reinterpret_cast<float4*>(v + e) = vv;
+  stream_store(reinterpret_cast<float4*>(x + e), xv);
+  if constexpr (KIND >= 1) stream_store(reinterpret_cast<float4*>(m + e), mv);
+  if constexpr (KIND == 2) stream_store(reinterpret_cast<float4*>(v + e), vv);
 }
 
 template <int KIND>

@@ -169,7 +169,7 @@ __device__ __forceinline__ void sketch_rows(
       } else {
         xv[u] = buffer_load_f4<kCacheNonTemporal>(rx, o);
       }
-      hv[u] = buffer_load_f4<kCacheDefault>(rh, o);
+      hv[u] = buffer_load_f4<kCacheNonTemporal>(rh, o);
       gv[u] = buffer_load_f4<kCacheNonTemporal>(rg, o);
     }
   };
