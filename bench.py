@@ -323,7 +323,8 @@ def main():
     comm = table1_communication(w, comp, args.compressor)
     sk_ms = stages["sketch"]
     achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
-    traffic = kernel_traffic(w)
+    # The committed counters cover the ARC sketch kernel only.
+    traffic = kernel_traffic(w) if args.compressor == "arc" else None
     value = w.N * w.d / (ms_per_step * 1e-3)
     step_gbps = byt["step"] / (ms_per_step * 1e-3) / 1e9
 
