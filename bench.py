@@ -134,31 +134,39 @@ def cpu_baseline(w, grads_dev, seconds_target=12.0):
     import oracle
     threads = oracle.num_threads()
 
-    def run(elems, steps):
+    def run(elems, steps=None, budget=None):
+        """Oracle steps on the first `elems` coordinates: `steps` of them, or
+        as many as `budget` seconds take (at least 2, at most 16).  The
+        gradients cycle through up to four host copies of the device batches."""
         d_s, kw, desc = _prefix(w, elems)
         h = np.zeros((w.N, d_s), np.float32)
         g = np.zeros((w.N, d_s), np.float32)
         grads = []
-        for s in range(steps):
+        for s in range(min(len(grads_dev), steps or 4)):
             gd = grads_dev[s % len(grads_dev)][:, :d_s].contiguous().cpu().numpy()
             grads.append(gd.view(np.uint16) if w.grad_dtype == "bf16" else gd)
-        t0 = time.perf_counter()
-        for s in range(steps):
+        done, t0 = 0, time.perf_counter()
+        while True:
             if w.per_tensor:
-                oracle.step_tensors(h, g, grads[s], kw["tensors"], r=w.r, eta=w.eta,
-                                    seed=w.sketch_seed, t=s)
+                oracle.step_tensors(h, g, grads[done % len(grads)], kw["tensors"], r=w.r,
+                                    eta=w.eta, seed=w.sketch_seed, t=done)
             else:
-                oracle.step(h, g, grads[s], r=w.r, eta=w.eta, seed=w.sketch_seed, t=s, **kw)
-        return (time.perf_counter() - t0) / steps, d_s, desc
+                oracle.step(h, g, grads[done % len(grads)], r=w.r, eta=w.eta,
+                            seed=w.sketch_seed, t=done, **kw)
+            done += 1
+            elapsed = time.perf_counter() - t0
+            if steps is not None and done >= steps:
+                break
+            if budget is not None and ((done >= 2 and elapsed >= budget) or done >= 16):
+                break
+        return elapsed / done, d_s, desc, done
 
-    # calibrate on a small prefix, then size the sample to the time target
-    t1, d1, _ = run(1 << 22, 1)
+    # calibrate on a small prefix, then size the sample so that two steps
+    # take about the time target, and run steps until it is spent
+    t1, d1, _, _ = run(1 << 22, steps=1)
     per_elem = t1 / d1
-    steps = 2
-    elems = int(min(w.d, max(d1, seconds_target / steps / max(per_elem, 1e-15))))
-    if elems >= w.d:  # whole workload fits the time budget: spend it on more steps
-        steps = int(max(2, min(8, seconds_target / max(per_elem * w.d, 1e-9))))
-    t_step, d_s, desc = run(elems, steps)
+    elems = int(min(w.d, max(d1, seconds_target / 2 / max(per_elem, 1e-15))))
+    t_step, d_s, desc, steps = run(elems, budget=seconds_target)
     return {
         "value": w.N * d_s / t_step,
         "unit": "gradient elements/s",
