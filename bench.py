@@ -37,9 +37,10 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w, K_total, compressor="arc"):
+def algorithmic_bytes(w, K_total, compressor="arc", fused=False):
     """Bytes the method must move per step (each array touched once).
-    sketch_kernel: the first (streaming) stage of the step."""
+    sketch_kernel: the first (streaming) stage of the step; fused: that stage
+    also writes the importance (the fused kernel, fewer than 4 workers)."""
     bg = w.bytes_per_grad
     Nd = w.N * w.d
     payload = w.payload_elems()
@@ -56,7 +57,11 @@ def algorithmic_bytes(w, K_total, compressor="arc"):
         return {"sketch_kernel": stream, "step": stream + select + gather + 4 * K_total}
     stream = Nd * (bg + 12)                         # grad + h read/write + g read
     sketch_out = 4 * w.N * w.m * w.r                # per-worker sketch written
-    reduce_ = 4 * w.N * w.m * w.r + 4 * w.m         # sketch read, importance written
+    if fused:                                       # importance written by the same kernel
+        sketch_out += 4 * w.m
+        reduce_ = 0
+    else:
+        reduce_ = 4 * w.N * w.m * w.r + 4 * w.m     # sketch read, importance written
     select = 4 * 4 * w.m                            # importance read by 4 passes
     gather = payload * (12 * w.N + 4)               # h, g read, g written, agg written
     return {"sketch_kernel": stream + sketch_out, "step": stream + sketch_out + reduce_ +
@@ -327,7 +332,8 @@ def main():
     stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
     log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
 
-    byt = algorithmic_bytes(w, comp.K_total, args.compressor)
+    comp_desc = comp.describe()
+    byt = algorithmic_bytes(w, comp.K_total, args.compressor, "sketch=fused" in comp_desc)
     comm = table1_communication(w, comp, args.compressor)
     sk_ms = stages["sketch"]
     achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
@@ -346,7 +352,6 @@ def main():
         log("[bench] cpu baseline (oracle) ...")
         cpu = cpu_baseline(w, grads)
         log(f"[bench] cpu baseline {cpu['value']:.3e} elements/s on {cpu['cores']} threads")
-    comp_desc = comp.describe()
     comp.close()
 
     out = {
