@@ -173,9 +173,16 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  *   ARC_COMP_TOPK: out_idx is [N][K] (node i's rows at [i*K, (i+1)*K)) and
  *            out_agg [N][L] (node i's rows of Delta^(i), laid out as above),
  *            with K and L one node's row count and payload length.
- * out_idx / out_agg may be NULL only when no row is kept.  Pointers 16-byte aligned with d % 4 == 0 and row widths
- * that are multiples of 32 take the vectorised path; anything else takes a
- * slower path with identical results.
+ * out_idx / out_agg may be NULL only when no row is kept.  With grad, h and
+ * g 16-byte aligned, d % 4 == 0 and r in {1, 2, 4, 8}, rows whose width is a
+ * multiple of 4 (per tensor: tensors that also start at a multiple of 4
+ * coordinates) take the vectorised path; anything else takes a slower path
+ * with identical results.
+ * The call returns once the work is queued on the context's stream.  On the
+ * host it generates V_t (ARC_COMP_ARC; V_{t+1} is then prepared in the
+ * background for the next call) and waits until the device has read the
+ * projection staged two calls earlier, so it cannot be captured into a HIP
+ * graph.
  */
 arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
                     float *g, int32_t *out_idx, float *out_agg);
