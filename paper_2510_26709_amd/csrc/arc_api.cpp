@@ -482,10 +482,11 @@ arc_status record(arc_ctx* c, size_t slot, int which) {
   return ARC_OK;
 }
 
-// Host threads for the projection: one per 16K values (a few hundred
-// microseconds of Box-Muller each), at most 8 and at most half the cores.
+// Host threads for the projection: one per 8K values (a few hundred
+// microseconds of Box-Muller each, well under a step of the device), at most
+// 8 and at most half the cores.
 int projection_threads(int64_t v_floats) {
-  const int64_t by_size = 1 + v_floats / 16384;
+  const int64_t by_size = 1 + v_floats / 8192;
   const int64_t cores = static_cast<int64_t>(std::thread::hardware_concurrency());
   const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(8, cores / 2));
   return static_cast<int>(std::min(by_size, cap));
