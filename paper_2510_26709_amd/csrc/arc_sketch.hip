@@ -327,8 +327,9 @@ sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
 }
 
 // ---------------------------------------------------------------------------
-// Per-worker path (more workers than one block holds): same streaming, one
-// wave per (row group, worker), sketch written to S for the reduce kernel.
+// Per-worker path (4 or more workers): same streaming, one wave per (row
+// group, worker), kSketchWaves groups of one worker per block, sketch written
+// to S for the reduce kernel.
 // ---------------------------------------------------------------------------
 constexpr int kSketchWaves = 4;
 
