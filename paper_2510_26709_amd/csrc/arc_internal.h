@@ -247,7 +247,7 @@ class ProjectionPool {
   void wait();
 
  private:
-  void run(int id);
+  void run(int id, int nthreads);
   std::vector<std::thread> threads_;
   std::mutex mu_;
   std::condition_variable cv_job_, cv_done_;

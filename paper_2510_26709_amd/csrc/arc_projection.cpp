@@ -71,7 +71,10 @@ void generate_projection(uint64_t seed, int64_t t, int64_t n, int32_t r, float* 
 // ---------------------------------------------------------------------------
 ProjectionPool::ProjectionPool(int threads) {
   if (threads < 1) threads = 1;
-  for (int i = 0; i < threads; ++i) threads_.emplace_back([this, i] { run(i); });
+  // Each thread gets the count by value: threads_ is still growing while the
+  // first ones start.
+  threads_.reserve(static_cast<size_t>(threads));
+  for (int i = 0; i < threads; ++i) threads_.emplace_back([this, i, threads] { run(i, threads); });
 }
 
 ProjectionPool::~ProjectionPool() {
@@ -104,9 +107,8 @@ void ProjectionPool::wait() {
   cv_done_.wait(lk, [this] { return remaining_ == 0; });
 }
 
-void ProjectionPool::run(int id) {
+void ProjectionPool::run(int id, int nthreads) {
   uint64_t seen = 0;
-  const int nthreads = static_cast<int>(threads_.size());
   for (;;) {
     std::unique_lock<std::mutex> lk(mu_);
     cv_job_.wait(lk, [&] { return quit_ || job_ != seen; });
