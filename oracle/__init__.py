@@ -15,7 +15,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# ARC_ORACLE_LIB selects another build of the same source (the sanitizer
+# test loads an instrumented copy this way).
+_LIB_PATH = os.environ.get("ARC_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _i32, _i64, _u64, _f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
