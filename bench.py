@@ -355,7 +355,7 @@ def main():
     comp.close()
 
     out = {
-        "metric": "arc_step gradient elements/s (1 MI355X)",
+        "metric": "arc_step gradient elements/s and achieved HBM GB/s (% of peak), 1 MI355X",
         "value": value,
         "unit": "gradient elements/s",
         "n_gpus": 1,
