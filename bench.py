@@ -250,6 +250,10 @@ def main():
                     help="ARC-Top-K, or a comparison compressor of Table I in the same step")
     ap.add_argument("--batches", type=int, default=4,
                     help="distinct gradient batches kept resident and cycled")
+    ap.add_argument("--workers", type=int, default=0,
+                    help="override the workload's simulated worker count N (1: one "
+                         "rank's share of a multi-GPU run, the streaming stage at its "
+                         "real shape with nothing to sum over workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-model-step", action="store_true",
                     help="skip the extra timing of the full EF21M iteration with Adam")
@@ -277,6 +281,9 @@ def main():
     import synth
 
     w = synth.WORKLOADS[args.workload]
+    if args.workers > 0 and args.workers != w.N:
+        import dataclasses
+        w = dataclasses.replace(w, name=f"{w.name}_N{args.workers}", N=args.workers)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(dev)
