@@ -37,10 +37,9 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(w, K_total, compressor="arc", fused=False):
+def algorithmic_bytes(w, K_total, compressor="arc"):
     """Bytes the method must move per step (each array touched once).
-    sketch_kernel: the first (streaming) stage of the step; fused: that stage
-    also writes the importance (the fused kernel, fewer than 4 workers)."""
+    sketch_kernel: the first (streaming) stage of the step."""
     bg = w.bytes_per_grad
     Nd = w.N * w.d
     payload = w.payload_elems()
@@ -57,11 +56,7 @@ def algorithmic_bytes(w, K_total, compressor="arc", fused=False):
         return {"sketch_kernel": stream, "step": stream + select + gather + 4 * K_total}
     stream = Nd * (bg + 12)                         # grad + h read/write + g read
     sketch_out = 4 * w.N * w.m * w.r                # per-worker sketch written
-    if fused:                                       # importance written by the same kernel
-        sketch_out += 4 * w.m
-        reduce_ = 0
-    else:
-        reduce_ = 4 * w.N * w.m * w.r + 4 * w.m     # sketch read, importance written
+    reduce_ = 4 * w.N * w.m * w.r + 4 * w.m         # sketch read, importance written
     select = 4 * 4 * w.m                            # importance read by 4 passes
     gather = payload * (12 * w.N + 4)               # h, g read, g written, agg written
     return {"sketch_kernel": stream + sketch_out, "step": stream + sketch_out + reduce_ +
@@ -340,7 +335,7 @@ def main():
     log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
 
     comp_desc = comp.describe()
-    byt = algorithmic_bytes(w, comp.K_total, args.compressor, "sketch=fused" in comp_desc)
+    byt = algorithmic_bytes(w, comp.K_total, args.compressor)
     comm = table1_communication(w, comp, args.compressor)
     sk_ms = stages["sketch"]
     achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
@@ -387,10 +382,9 @@ def main():
         "path": comp_desc,
         "roofline": {
             "bound": "hbm",
-            "kernel": {"arc": "sketch stage: sketch_per_worker_kernel (4 or more workers) "
-                              "or sketch_fused_kernel (fewer; also the worker sum and "
-                              "importance) launches, momentum + residual + sketch, plus the "
-                              "general-row kernels where the layout has any",
+            "kernel": {"arc": "sketch stage: sketch_per_worker_kernel launches (momentum + "
+                              "residual + per-worker sketch), plus the general-row kernel "
+                              "where the layout has any",
                        "randk": "momentum_vec_kernel (Eq. (11a) over N*d)",
                        "topk": "row-norm stage: sketch_per_worker_kernel in norm mode "
                                "(momentum + residual + per-node squared row norms)",

@@ -46,7 +46,6 @@ arc_status fail_hip(hipError_t e, const char* where) {
   } while (0)
 
 constexpr int kEventsPerStep = 6;
-constexpr int32_t kPerWorkerFromWorkers = 4;  // see arc_ctx::use_fused
 constexpr int64_t kGroupRows = 64;  // rows of one row group (one wave's rows)
 constexpr int32_t kMaxTensors = 1 << 24;
 
@@ -145,17 +144,6 @@ struct arc_ctx {
   bool timing = false;
   std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
   size_t ev_used = 0;
-
-  // The fused sketch kernel streams the N workers' copies of the same rows
-  // in one block; the per-worker kernel streams consecutive row groups of
-  // one worker per block and leaves the worker sum to a small reduce kernel.
-  // Measured on one MI355X: with 2 workers fused is faster (7B layout 31.9
-  // vs 32.5 ms), with 4 the per-worker order is (1.1B 11.47 vs 11.7-11.85
-  // ms, per-tensor 1.1B 11.77 vs 12.37 ms), with 8 they tie (GPT-2 small).
-  bool use_fused() const {
-    return N < kPerWorkerFromWorkers && N <= arc::kMaxFusedWorkers &&
-           arc::fused_sketch_lds_bytes(N) <= max_lds_per_block;
-  }
 
   arc::SelectWorkspace select_ws() const {
     arc::SelectWorkspace ws;
@@ -698,14 +686,13 @@ arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const 
   return ARC_OK;
 }
 
-// The streaming stage (S1-S3, plus S4 for the fused kernel; norm: Top-K's
-// row norms): one launch per row-group size present and one for the general
-// groups.  When there are several, the one over the most coordinates runs on
+// The streaming stage (S1-S3; norm: Top-K's row norms): one launch per
+// row-group size present and one for the general groups.  When there are several, the one over the most coordinates runs on
 // the caller's stream and the others on the second stream, forked after
 // everything queued before and joined before anything queued after, so that
 // they overlap it instead of following it.
 arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const float* g,
-                                  int64_t nvec, int64_t ngroups, bool fused, bool norm) {
+                                  int64_t nvec, int64_t ngroups, bool norm) {
   int which[5], nl = 0, big = 0;
   for (int sz = 0; sz < 4; ++sz)
     if (nvec > 0 && c->vec_count[sz] > 0) which[nl++] = sz;
@@ -745,11 +732,6 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
                                       c->vec_count[w], c->S_dev, c->d, c->m, c->N, c->eta, c->a,
                                       s),
                 "row norm launch");
-      } else if (fused) {
-        ARC_HIP(arc::launch_sketch_fused(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
-                                         c->vec_count[w], c->S_dev, c->sigma_dev, c->d, c->m,
-                                         c->N, c->r, c->eta, c->a, s),
-                "fused sketch launch");
       } else {
         ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
                                               c->vec_count[w], c->S_dev, c->d, c->m, c->N,
@@ -773,7 +755,6 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   // are 16-byte aligned; otherwise every group takes the general kernel.
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
   const int64_t nvec = aligned16(grad) && aligned16(h) && aligned16(g) ? c->nvec_groups : 0;
-  const bool fused = nvec > 0 && c->use_fused();
 
   size_t slot = 0;
   if (c->timing) {
@@ -803,7 +784,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
     if ((st = record(c, slot, 4))) return st;
   } else if (c->compressor == ARC_COMP_TOPK) {
     // Stage 0: Eq. (11a) with every node's squared row norms of Delta.
-    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, false, true))) return st;
+    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, true))) return st;
     if ((st = record(c, slot, 2))) return st;
     if ((st = record(c, slot, 3))) return st;
     // Stage 2: every node's own top-K over its norms.
@@ -819,19 +800,17 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
             "gather launch");
     return record(c, slot, 5);
   } else {
-    // Stage 0: momentum + residual + sketch in one HBM stream.  With N <= 8
-    // the fused kernel also forms the worker sum and importance of its rows.
-    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, fused, false))) return st;
+    // Stage 0: momentum + residual + per-worker sketch in one HBM stream.
+    // Measured on one MI355X, this order (one worker's row groups per block,
+    // then the reduce kernel) is as fast as or faster than streaming the N
+    // workers' copies of a group in one block and summing them in LDS, for
+    // every worker count: 7B with 2 workers 33.5-34.0 vs 34.4-34.7 ms, 1.1B
+    // with 1 worker 2.94 vs 3.00 ms, with 2 equal.
+    if ((st = launch_streaming_stage(c, grad, h, g, nvec, ngroups, false))) return st;
     if ((st = record(c, slot, 2))) return st;
-    // Stage 1: worker sum + importance of the rows the fused kernel did not
-    // do: the general groups' rows, or every row.
-    if (fused)
-      ARC_HIP(arc::launch_reduce_importance(c->S_dev, c->sigma_dev, c->groups_dev + nvec,
-                                            ngroups - nvec, c->m, c->N, c->r, c->stream),
-              "reduce launch");
-    else
-      ARC_HIP(arc::launch_reduce_rows(c->S_dev, c->sigma_dev, c->m, c->N, c->r, c->stream),
-              "reduce launch");
+    // Stage 1: worker sum + importance of every row.
+    ARC_HIP(arc::launch_reduce_rows(c->S_dev, c->sigma_dev, c->m, c->N, c->r, c->stream),
+            "reduce launch");
     if ((st = record(c, slot, 3))) return st;
     // Stage 2: per-bucket top-K.
     ARC_HIP(arc::launch_select(c->sigma_dev, ws, out_idx, c->stream), "select launch");
@@ -957,13 +936,12 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
   const char* sketch = c->compressor == ARC_COMP_RANDK ? "none"
                        : c->nvec_groups == 0           ? "general"
                        : c->compressor == ARC_COMP_TOPK ? "row_norms"
-                       : c->use_fused()                ? "fused"
                                                        : "per_worker+reduce";
   int radix = 0;
   for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
   std::snprintf(buf, static_cast<size_t>(len),
                 "compressor=%s mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
-                "(64:%lld 32:%lld 16:%lld 8:%lld rows) general_groups=%lld fused_lds_bytes=%zu "
+                "(64:%lld 32:%lld 16:%lld 8:%lld rows) general_groups=%lld "
                 "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld "
                 "payload=%lld",
                 comp, c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
@@ -971,7 +949,7 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
                 static_cast<long long>(c->vec_count[0]), static_cast<long long>(c->vec_count[1]),
                 static_cast<long long>(c->vec_count[2]), static_cast<long long>(c->vec_count[3]),
                 static_cast<long long>(ngroups - c->nvec_groups),
-                arc::fused_sketch_lds_bytes(c->N), c->max_lds_per_block, c->buckets.size(),
+                c->max_lds_per_block, c->buckets.size(),
                 radix, c->blocks.size(), static_cast<long long>(c->K_total),
                 static_cast<long long>(c->payload));
   return ARC_OK;

@@ -12,8 +12,6 @@
 
 namespace arc {
 
-// Workers one block of the fused sketch kernel can hold (one wave each).
-constexpr int kMaxFusedWorkers = 8;
 
 // Selection kernels: 256 threads per block; radix digits over the 32 key bits
 // [31:21], [20:10], [9:0].
@@ -103,28 +101,14 @@ constexpr int64_t kSmallBucketRows = 8 * kSmallSelectThreads;
 
 // ---- launchers; each returns hipGetLastError() ----
 
-// Bytes of LDS one block of the fused sketch kernel uses for N workers.
-size_t fused_sketch_lds_bytes(int32_t N);
-
 // Row groups of group_rows rows take chunks of vector_chunk_cols(group_rows)
 // columns in the vectorised sketch kernels.
 constexpr int32_t vector_chunk_cols(int32_t group_rows) { return 2048 / group_rows; }
 
-// Momentum + residual + per-worker sketch + worker sum + importance for the
-// row groups groups[0 .. ngroups): one block per group holding all N <= 8
-// workers.  Every group must be vectorisable for group_rows in {64, 32, 16}:
-// at most group_rows rows, cols a multiple of vector_chunk_cols(group_rows),
-// 16-byte aligned rows, r in {1,2,4,8}, no ragged tail, rows*cols*4 < 2^31.
-hipError_t launch_sketch_fused(int32_t group_rows, const void* grad, int32_t grad_bf16,
-                               float* h,
-                               const float* g, const float* V,
-                               const RowGroup* groups, int64_t ngroups,
-                               float* S, float* sigma, int64_t d, int64_t m,
-                               int32_t N, int32_t r, float eta, float a,
-                               hipStream_t stream);
-
-// Momentum + residual + per-worker sketch into S for groups[0 .. ngroups),
-// vectorisable groups (as for the fused kernel), any N.
+// Momentum + residual + per-worker sketch into S for the row groups
+// groups[0 .. ngroups), any N.  Every group must be vectorisable for
+// group_rows in {64, 32, 16, 8}: at most group_rows rows, cols a multiple of
+// 4 and at most 2^22, 16-byte aligned rows, r in {1, 2, 4, 8}.
 hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_t grad_bf16,
                                     float* h, const float* g, const float* V,
                                     const RowGroup* groups, int64_t ngroups, float* S,
@@ -165,13 +149,8 @@ hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int3
                               int64_t work, int64_t K_total, int64_t payload, int64_t d,
                               int64_t m, int32_t N, bool vec, hipStream_t stream);
 
-// P = sum_i S[i] (ascending i), sigma = row norm squared of P, for the rows
-// of groups[0 .. ngroups).
-hipError_t launch_reduce_importance(const float* S, float* sigma,
-                                    const RowGroup* groups, int64_t ngroups,
-                                    int64_t m, int32_t N, int32_t r,
-                                    hipStream_t stream);
-// The same for every row 0 .. m-1 (one thread per row).
+// P = sum_i S[i] (ascending i), sigma = row norm squared of P, for every row
+// 0 .. m-1 (one thread per row).
 hipError_t launch_reduce_rows(const float* S, float* sigma, int64_t m, int32_t N, int32_t r,
                               hipStream_t stream);
 

@@ -1,6 +1,7 @@
 // Streaming stage of the compressor step: EF21M momentum (11a), residual
-// Delta = h_t - g_{t-1}, per-worker sketch P^(i) = G^(i) V (Alg. 1), worker
-// sum and row importance Sigma = diag(P P^T) (Eq. (4)).
+// Delta = h_t - g_{t-1} and per-worker sketch P^(i) = G^(i) V (Alg. 1) in one
+// pass over HBM; then the worker sum and row importance Sigma = diag(P P^T)
+// (Eq. (4)) in a small kernel over the sketches.
 //
 // Numerics follow the contract in libarctopk.h: binary32; the dot product of
 // a row with column k of V is a fused multiply-add chain in ascending column
@@ -53,7 +54,6 @@ constexpr int slice_f4() {
 }
 template <int R, int G, bool NORM>
 constexpr int wave_lds_f4() { return kTileF4 + slice_f4<R, G, NORM>(); }
-constexpr int kMaxWaveLdsF4 = kTileF4 + 520;  // largest slice: R = 8, G = 8, transposed
 // Offset whose access the hardware drops: a group spans at most 2^30 bytes
 // (64 rows of at most 2^22 binary32 values), so 2^31, and the 2^30 it becomes
 // for the bf16 stream's halved offsets, lie beyond every resource here.
@@ -279,57 +279,10 @@ __device__ __forceinline__ void sketch_rows(
 }
 
 // ---------------------------------------------------------------------------
-// Fused path: a block is N waves, wave i streams worker i over the same row
-// group; the waves then meet in LDS and wave 0 forms P = S^(0) + S^(1) + ...
-// (ascending worker order) and Sigma for the group's rows.  Sketches never leave
-// the chip except as the per-worker copy S kept for inspection.
-// HBM traffic per element and worker: grad (4 or 2 B) + h read and write
-// (8 B) + g read (4 B).
-// ---------------------------------------------------------------------------
-template <int R, bool BF16, int G>
-__global__ void __launch_bounds__(kMaxFusedWorkers * kWave)
-sketch_fused_kernel(const void* __restrict__ grad, float* __restrict__ h,
-                    const float* __restrict__ g, const float* __restrict__ V,
-                    const RowGroup* __restrict__ groups, float* __restrict__ S,
-                    float* __restrict__ sigma, int64_t d, int64_t m, int32_t N,
-                    float eta, float a) {
-  extern __shared__ float4 lds_tiles[];  // N wave areas of wave_lds_f4 float4
-  constexpr int kWaveF4 = wave_lds_f4<R, G, false>();
-  const int lane = threadIdx.x & (kWave - 1);
-  const int i = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // worker
-  const RowGroup grp = groups[xcd_contiguous_block(blockIdx.x, gridDim.x)];
-  float4* tile = lds_tiles + i * kWaveF4;
-  float s[R];
-  sketch_rows<R, BF16, G>(grad, h, g, V, d, grp, i, eta, a, tile, s);
-  const bool mine = lane < grp.rows;
-  const int64_t p = grp.row0 + lane;
-  if (mine) {
-    float* out = S + ((int64_t)i * m + p) * R;
-#pragma unroll
-    for (int k = 0; k < R; ++k) out[k] = s[k];
-  }
-  __syncthreads();  // every wave is done with its tile
-  float* comb = reinterpret_cast<float*>(tile);
-#pragma unroll
-  for (int k = 0; k < R; ++k) comb[k * kWave + lane] = s[k];
-  __syncthreads();
-  if (i == 0 && mine) {
-    const float* base = reinterpret_cast<const float*>(lds_tiles);
-    float acc = 0.0f;
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-      float P = s[k];
-      for (int32_t w = 1; w < N; ++w) P = P + base[w * kWaveF4 * 4 + k * kWave + lane];
-      acc = fmaf(P, P, acc);
-    }
-    sigma[p] = acc;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Per-worker path (4 or more workers): same streaming, one wave per (row
-// group, worker), kSketchWaves groups of one worker per block, sketch written
-// to S for the reduce kernel.
+// One wave per (row group, worker), kSketchWaves groups of one worker per
+// block; the sketch goes to S for the reduce kernel (4r bytes per row and
+// worker).  HBM traffic per element and worker: grad (4 or 2 B) + h read and
+// write (8 B) + g read (4 B).  Delta never leaves the chip.
 // ---------------------------------------------------------------------------
 constexpr int kSketchWaves = 4;
 
@@ -384,16 +337,6 @@ __device__ __forceinline__ void reduce_row(const float* __restrict__ S, float* _
   sigma[p] = acc;
 }
 
-// For the rows of groups[0 .. ngroups): one 64-thread block per group, one
-// thread per row.
-__global__ void __launch_bounds__(kWave)
-reduce_importance_kernel(const float* __restrict__ S, float* __restrict__ sigma,
-                         const RowGroup* __restrict__ groups, int64_t m, int32_t N,
-                         int32_t r) {
-  const RowGroup grp = groups[blockIdx.x];
-  if ((int32_t)threadIdx.x < grp.rows) reduce_row(S, sigma, grp.row0 + threadIdx.x, m, N, r);
-}
-
 // For every row: one thread per row.
 __global__ void __launch_bounds__(256)
 reduce_rows_kernel(const float* __restrict__ S, float* __restrict__ sigma, int64_t m, int32_t N,
@@ -401,26 +344,6 @@ reduce_rows_kernel(const float* __restrict__ S, float* __restrict__ sigma, int64
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p < m) reduce_row(S, sigma, p, m, N, r);
 }
-
-}  // namespace
-
-size_t fused_sketch_lds_bytes(int32_t N) {
-  return (size_t)N * kMaxWaveLdsF4 * sizeof(float4);
-}
-
-namespace {
-
-template <int R, bool BF16, int G>
-struct FusedLaunch {
-  static void run(const void* grad, float* h, const float* g, const float* V,
-                  const RowGroup* groups, int64_t ngroups, float* S, float* sigma,
-                  int64_t d, int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
-    constexpr size_t kWaveBytes = wave_lds_f4<R, G, false>() * sizeof(float4);
-    hipLaunchKernelGGL((sketch_fused_kernel<R, BF16, G>), dim3((unsigned)ngroups),
-                       dim3(N * kWave), N * kWaveBytes, stream, grad, h, g, V, groups, S,
-                       sigma, d, m, N, eta, a);
-  }
-};
 
 template <int R, bool BF16, int G>
 struct PerWorkerLaunch {
@@ -463,20 +386,6 @@ bool dispatch(int32_t r, bool bf16, int32_t group_rows, Args... args) {
 }
 
 }  // namespace
-
-hipError_t launch_sketch_fused(int32_t group_rows, const void* grad, int32_t grad_bf16,
-                               float* h, const float* g, const float* V,
-                               const RowGroup* groups, int64_t ngroups,
-                               float* S, float* sigma, int64_t d, int64_t m,
-                               int32_t N, int32_t r, float eta, float a,
-                               hipStream_t stream) {
-  if (ngroups <= 0) return hipSuccess;
-  if (N < 1 || N > kMaxFusedWorkers) return hipErrorInvalidValue;
-  if (!dispatch<FusedLaunch>(r, grad_bf16 != 0, group_rows, grad, h, g, V, groups, ngroups, S,
-                             sigma, d, m, N, eta, a, stream))
-    return hipErrorInvalidValue;
-  return hipGetLastError();
-}
 
 hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_t grad_bf16,
                                     float* h, const float* g, const float* V,
@@ -522,16 +431,6 @@ hipError_t launch_reduce_rows(const float* S, float* sigma, int64_t m, int32_t N
   if (m <= 0) return hipSuccess;
   hipLaunchKernelGGL(reduce_rows_kernel, dim3(blocks_for(m, 256)), dim3(256), 0, stream, S,
                      sigma, m, N, r);
-  return hipGetLastError();
-}
-
-hipError_t launch_reduce_importance(const float* S, float* sigma,
-                                    const RowGroup* groups, int64_t ngroups,
-                                    int64_t m, int32_t N, int32_t r,
-                                    hipStream_t stream) {
-  if (ngroups <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_importance_kernel, dim3((unsigned)ngroups), dim3(kWave), 0,
-                     stream, S, sigma, groups, m, N, r);
   return hipGetLastError();
 }
 

@@ -23,12 +23,6 @@ def test_algorithmic_bytes_of_the_streaming_stage():
     w = synth.WORKLOADS["gpt2s"]
     assert bench.algorithmic_bytes(w, w.K_global())["sketch_kernel"] == \
         w.N * w.d * 16 + 4 * w.N * w.m * w.r
-    # fused kernel: the importance is written by the same launch, no reduce
-    w = synth.WORKLOADS["llama7b"]
-    fused = bench.algorithmic_bytes(w, 1, fused=True)
-    plain = bench.algorithmic_bytes(w, 1)
-    assert fused["sketch_kernel"] == plain["sketch_kernel"] + 4 * w.m
-    assert fused["step"] == plain["step"] - 4 * w.N * w.m * w.r
 
 
 def test_comparison_compressors_stream_what_they_need():

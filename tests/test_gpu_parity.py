@@ -47,7 +47,7 @@ CASES = [
                              family=1)),
     ("bf16_per_worker_N9", dict(d=128 * 500, N=9, n=128, r=4, K=6, steps=2, grad_dtype="bf16",
                                 family=1)),
-    ("bf16_fused_r8_N2", dict(d=64 * 3000, N=2, n=64, r=8, K=40, steps=2, grad_dtype="bf16",
+    ("bf16_r8_N2", dict(d=64 * 3000, N=2, n=64, r=8, K=40, steps=2, grad_dtype="bf16",
                               family=1)),
     ("select_many_blocks", dict(d=32 * 300_000, N=1, n=32, r=4, K=150_000, steps=1)),
     ("generic_r32_max", dict(d=40 * 500 + 13, N=3, n=40, r=32, K=7, steps=2)),
@@ -55,26 +55,26 @@ CASES = [
                               family=1)),
     ("generic_wide_ragged", dict(d=1000 * 70 + 999, N=3, n=1000, r=4, K=5, steps=2)),
     ("generic_many_workers", dict(d=50 * 257, N=11, n=50, r=4, K=20, steps=2)),
-    # fused kernel (N <= 3) and per-worker kernel (N >= 4) for every r and
+    # the sketch kernel with 2 to 6 workers for every r and
     # row-group size (8 rows for n % 256 == 0, 16 for n % 128, 32 for n % 64,
     # 64 otherwise)
-    ("fused_r2_g64", dict(d=96 * 513, N=2, n=96, r=2, K=7, steps=2)),
-    ("fused_g32_bf16", dict(d=192 * 400, N=3, n=192, r=4, K=9, steps=2, grad_dtype="bf16",
+    ("r2_g64_N2", dict(d=96 * 513, N=2, n=96, r=2, K=7, steps=2)),
+    ("g32_bf16_N3", dict(d=192 * 400, N=3, n=192, r=4, K=9, steps=2, grad_dtype="bf16",
                             family=1)),
     ("per_worker_g32", dict(d=192 * 500, N=4, n=192, r=4, K=9, steps=2)),
     ("per_worker_r8_g64", dict(d=32 * 4097, N=4, n=32, r=8, K=100, steps=2)),
     ("per_worker_r1_bf16", dict(d=128 * 777, N=5, n=128, r=1, K=30, steps=2, grad_dtype="bf16",
                                 family=1)),
-    ("fused_g8_r8_bf16", dict(d=256 * 700 + 36, N=3, n=256, r=8, K=9, steps=2, grad_dtype="bf16",
+    ("g8_r8_bf16_N3", dict(d=256 * 700 + 36, N=3, n=256, r=8, K=9, steps=2, grad_dtype="bf16",
                               family=1)),
     ("per_worker_g8_r2", dict(d=512 * 400, N=6, n=512, r=2, K=9, steps=2)),
-    ("fused_g16_r4", dict(d=128 * 900, N=2, n=128, r=4, K=9, steps=2)),
+    ("g16_r4_N2", dict(d=128 * 900, N=2, n=128, r=4, K=9, steps=2)),
     # widths that are multiples of 4 but not of the chunk: every row's last
     # chunk is partial (32 + 4, 64 + 36, 7 x 128 + 104 columns), and the
     # ragged tail row is a one-row vector group as wide as its values
-    ("partial_chunk_g64_bf16_fused", dict(d=36 * 900 + 20, N=2, n=36, r=8, K=40, steps=2,
+    ("partial_chunk_g64_bf16_N2", dict(d=36 * 900 + 20, N=2, n=36, r=8, K=40, steps=2,
                                           grad_dtype="bf16", family=1)),
-    ("partial_chunk_g32_fused", dict(d=100 * 321 + 8, N=3, n=100, r=4, K=12, steps=3)),
+    ("partial_chunk_g32_N3", dict(d=100 * 321 + 8, N=3, n=100, r=4, K=12, steps=3)),
     ("partial_chunk_g16_bf16_per_worker", dict(d=1000 * 80 + 996, N=4, n=1000, r=4, K=5, steps=2,
                                                grad_dtype="bf16", family=1)),
     ("partial_chunk_n4_per_worker", dict(d=4 * 5000, N=5, n=4, r=2, K=60, steps=2)),
@@ -89,7 +89,8 @@ def test_parity_small(name, kw):
 
 
 def test_describe_names_the_kernel_path():
-    for N, want in ((2, "sketch=fused"), (3, "sketch=fused"), (4, "sketch=per_worker+reduce"),
+    for N, want in ((1, "sketch=per_worker+reduce"), (3, "sketch=per_worker+reduce"),
+                    (4, "sketch=per_worker+reduce"),
                     (8, "sketch=per_worker+reduce"), (12, "sketch=per_worker+reduce")):
         comp = arc.Compressor(d=256 * 64, N=N, n=256, K=3, eta=0.1, seed=1)
         try:
@@ -108,7 +109,7 @@ def test_describe_names_the_kernel_path():
     comp = arc.Compressor(d=100 * 64 + 8, N=2, n=100, r=4, K=3, eta=0.1, seed=1)
     try:
         desc = comp.describe()
-        assert "sketch=fused" in desc and "general_groups=0" in desc, desc
+        assert "sketch=per_worker+reduce" in desc and "general_groups=0" in desc, desc
     finally:
         comp.close()
 
