@@ -72,9 +72,16 @@ bool vector_r(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8; }
 // 0.38 -> 0.35 ms, per-tensor ResNet-18 0.54 -> 0.51 ms, GPT-2 small
 // 3.06 -> 3.00 ms (per tensor 3.23 -> 3.17), TinyLlama 11.87 -> 11.60 ms
 // (per tensor 12.02 -> 11.70).
+// One measured exception: rows of exactly 2048 values stream faster in
+// 16-row groups (128-column chunks) than in 8-row ones (1.1B workload 11.10
+// vs 11.39 ms; binary32 gradients at that width 5.56 vs 5.77 ms), while at
+// 768, 1024 and 3072 values 8-row groups are 2-5% faster and at 4096 and
+// 5632 the two tie.
 constexpr int32_t kGroupSizes[] = {8, 16, 32, 64};
+constexpr int64_t kSixteenRowWidth = 2048;
 int32_t vector_group_rows(int64_t cols) {
   if (cols > (int64_t{1} << 22) || cols % 4 != 0) return 0;
+  if (cols == kSixteenRowWidth) return 16;
   for (int32_t gr : kGroupSizes)
     if (cols % arc::vector_chunk_cols(gr) == 0) return gr;
   for (int32_t gr : kGroupSizes)
