@@ -114,6 +114,7 @@ struct arc_ctx {
   int64_t nvec_groups = 0;
   std::array<int64_t, 4> vec_count{};  // groups of 64, 32, 16 and 8 rows
   std::array<int64_t, 5> stage_elems{};  // coordinates per launch: those sizes, general
+  std::array<arc::SketchOccupancy, 4> vec_occ{};  // launch shape per group size
   // per-tensor gather
   std::vector<arc::GatherBucket> gather;
   int64_t gather_work = 0;
@@ -303,6 +304,33 @@ int size_slot(int32_t group_rows) {
   return group_rows == 64 ? 0 : group_rows == 32 ? 1 : group_rows == 16 ? 2 : 3;
 }
 
+// Occupancy of one vectorised sketch launch from its groups' mean number of
+// chunks per row (weighted by coordinates).  A wave streams one chunk while
+// its chains run over the previous one; fewer waves per compute unit keep
+// fewer DRAM rows open at once, which the stage gains from as long as each
+// wave has enough chunks to keep its loads ahead of its chains.  Measured on
+// one MI355X (step ms, 4-wave workgroups at 3 per CU / 4 waves per CU /
+// 2 waves per CU): 2048-wide rows in 16-row groups (16 chunks) 11.37 / 10.69
+// / 10.09; 4096-wide in 8-row groups (16 chunks) 33.97 / 32.03 / 31.15;
+// 768-wide in 8-row groups (3 chunks) 2.88 / 2.76 / 2.93; 512-wide (2
+// chunks) 0.350 / 0.345 / 0.370; 256-wide (one chunk, a 50 MB working set)
+// 0.047 / 0.049 / 0.053.
+constexpr double kTwoWaveChunks = 9.0;
+arc::SketchOccupancy sketch_occupancy(const std::vector<arc::RowGroup>& groups,
+                                      int32_t group_rows) {
+  double elems = 0.0, weighted = 0.0;
+  const int64_t cw = arc::vector_chunk_cols(group_rows);
+  for (const arc::RowGroup& grp : groups) {
+    const double e = static_cast<double>(grp.rows) * grp.cols;
+    elems += e;
+    weighted += e * static_cast<double>((grp.cols + cw - 1) / cw);
+  }
+  const double chunks = elems > 0.0 ? weighted / elems : 0.0;
+  if (chunks >= kTwoWaveChunks) return {2, 1};
+  if (chunks >= 2.0) return {4, 1};
+  return {4, 0};
+}
+
 // Row groups over `rows` rows of width `cols` that start at coordinate
 // elem_off and global row row0; the last row holds last_len <= cols values.
 // group_rows > 0: vectorisable groups of that many rows (the view has no
@@ -443,6 +471,7 @@ void build_plan(const arc_config* cfg, arc_ctx* c) {
   c->groups.clear();
   for (int sz = 0; sz < 4; ++sz) {
     c->vec_count[sz] = static_cast<int64_t>(lists.vec[sz].size());
+    c->vec_occ[sz] = sketch_occupancy(lists.vec[sz], 64 >> sz);
     for (const arc::RowGroup& grp : lists.vec[sz])
       c->stage_elems[sz] += (grp.rows - 1) * static_cast<int64_t>(grp.cols) + grp.last_len;
     c->groups.insert(c->groups.end(), lists.vec[sz].begin(), lists.vec[sz].end());
@@ -596,6 +625,14 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   e = hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device);
   if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
   c->max_lds_per_block = static_cast<size_t>(lds_limit);
+  // One workgroup per compute unit is reached through the LDS reservation,
+  // which assumes the gfx950 figure; on any other, launches go uncapped.
+  int lds_cu = 0;
+  e = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                            c->device);
+  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
+  if (lds_cu != arc::kLdsPerCu || lds_limit < arc::kLdsPerCu / 2 + 1024)
+    for (auto& o : c->vec_occ) o.one_per_cu = 0;
 
   const size_t nb = c->buckets.size(), nblk = c->blocks.size();
   if ((st = dev_alloc(&c->V_dev, static_cast<size_t>(c->v_floats), "hipMalloc(V)")) ||
@@ -737,12 +774,12 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
       if (norm) {
         ARC_HIP(arc::launch_row_norms(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
                                       c->vec_count[w], c->S_dev, c->d, c->m, c->N, c->eta, c->a,
-                                      s),
+                                      c->vec_occ[w], s),
                 "row norm launch");
       } else {
         ARC_HIP(arc::launch_sketch_per_worker(gr, grad, c->grad_bf16, h, g, c->V_dev, grp,
                                               c->vec_count[w], c->S_dev, c->d, c->m, c->N,
-                                              c->r, c->eta, c->a, s),
+                                              c->r, c->eta, c->a, c->vec_occ[w], s),
                 "sketch launch");
       }
     }
@@ -948,13 +985,18 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
   for (const auto& b : c->buckets) radix += b.mode == arc::kSelectRadix;
   std::snprintf(buf, static_cast<size_t>(len),
                 "compressor=%s mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
-                "(64:%lld 32:%lld 16:%lld 8:%lld rows) general_groups=%lld "
+                "(64:%lld 32:%lld 16:%lld 8:%lld rows) workgroup_waves=(%d%s %d%s %d%s %d%s) "
+                "general_groups=%lld "
                 "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld "
                 "payload=%lld",
                 comp, c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
                 static_cast<long long>(ngroups), static_cast<long long>(c->nvec_groups),
                 static_cast<long long>(c->vec_count[0]), static_cast<long long>(c->vec_count[1]),
                 static_cast<long long>(c->vec_count[2]), static_cast<long long>(c->vec_count[3]),
+                c->vec_occ[0].waves, c->vec_occ[0].one_per_cu ? "/cu" : "",
+                c->vec_occ[1].waves, c->vec_occ[1].one_per_cu ? "/cu" : "",
+                c->vec_occ[2].waves, c->vec_occ[2].one_per_cu ? "/cu" : "",
+                c->vec_occ[3].waves, c->vec_occ[3].one_per_cu ? "/cu" : "",
                 static_cast<long long>(ngroups - c->nvec_groups),
                 c->max_lds_per_block, c->buckets.size(),
                 radix, c->blocks.size(), static_cast<long long>(c->K_total),

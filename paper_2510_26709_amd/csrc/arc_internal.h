@@ -105,6 +105,18 @@ constexpr int64_t kSmallBucketRows = 8 * kSmallSelectThreads;
 // columns in the vectorised sketch kernels.
 constexpr int32_t vector_chunk_cols(int32_t group_rows) { return 2048 / group_rows; }
 
+// LDS of one compute unit of the MI355X (gfx950).
+constexpr int32_t kLdsPerCu = 160 * 1024;
+
+// Shape of one launch of the vectorised sketch kernels: workgroups of `waves`
+// waves (2 or 4, one row group per wave), and, with one_per_cu, a dynamic LDS
+// reservation that makes every workgroup hold more than half of a compute
+// unit's LDS, so that at most one runs per compute unit.
+struct SketchOccupancy {
+  int32_t waves;
+  int32_t one_per_cu;
+};
+
 // Momentum + residual + per-worker sketch into S for the row groups
 // groups[0 .. ngroups), any N.  Every group must be vectorisable for
 // group_rows in {64, 32, 16, 8}: at most group_rows rows, cols a multiple of
@@ -113,7 +125,7 @@ hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_
                                     float* h, const float* g, const float* V,
                                     const RowGroup* groups, int64_t ngroups, float* S,
                                     int64_t d, int64_t m, int32_t N, int32_t r, float eta,
-                                    float a, hipStream_t stream);
+                                    float a, SketchOccupancy occ, hipStream_t stream);
 
 // The same for any row group (any width, r <= ARC_MAX_R, element alignment,
 // ragged last row), one wave per (group, worker).  norm (r = 1): S holds each
@@ -128,7 +140,7 @@ hipError_t launch_sketch_general(const void* grad, int32_t grad_bf16, float* h,
 hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_bf16, float* h,
                             const float* g, const float* V, const RowGroup* groups,
                             int64_t ngroups, float* norms, int64_t d, int64_t m, int32_t N,
-                            float eta, float a, hipStream_t stream);
+                            float eta, float a, SketchOccupancy occ, hipStream_t stream);
 
 // ---- comparison compressors (arc_compare.hip) ----
 

@@ -279,25 +279,23 @@ __device__ __forceinline__ void sketch_rows(
 }
 
 // ---------------------------------------------------------------------------
-// One wave per (row group, worker), kSketchWaves groups of one worker per
-// block; the sketch goes to S for the reduce kernel (4r bytes per row and
-// worker).  HBM traffic per element and worker: grad (4 or 2 B) + h read and
-// write (8 B) + g read (4 B).  Delta never leaves the chip.
+// One wave per (row group, worker), WAVES groups of one worker per workgroup;
+// the sketch goes to S for the reduce kernel (4r bytes per row and worker).
+// HBM traffic per element and worker: grad (4 or 2 B) + h read and write
+// (8 B) + g read (4 B).  Delta never leaves the chip.
 // ---------------------------------------------------------------------------
-constexpr int kSketchWaves = 4;
-
-template <int R, bool BF16, int G, bool NORM = false>
-__global__ void __launch_bounds__(kSketchWaves * kWave)
+template <int R, bool BF16, int G, int WAVES, bool NORM = false>
+__global__ void __launch_bounds__(WAVES * kWave)
 sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
                          const float* __restrict__ g, const float* __restrict__ V,
                          const RowGroup* __restrict__ groups, int64_t ngroups,
                          float* __restrict__ S, int64_t d, int64_t m, float eta,
                          float a) {
-  __shared__ float4 tiles[kSketchWaves][wave_lds_f4<R, G, NORM>()];
+  __shared__ float4 tiles[WAVES][wave_lds_f4<R, G, NORM>()];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t i = blockIdx.y;
-  const int64_t gi = xcd_contiguous_block(blockIdx.x, gridDim.x) * kSketchWaves + wave;
+  const int64_t gi = xcd_contiguous_block(blockIdx.x, gridDim.x) * WAVES + wave;
   if (gi >= ngroups) return;  // whole wave; no block barrier follows
   const RowGroup grp = groups[gi];
   float s[R];
@@ -307,6 +305,38 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
 #pragma unroll
     for (int k = 0; k < R; ++k) out[k] = s[k];
   }
+}
+
+// Launch over ngroups row groups and N workers.  With one_per_cu the launch
+// asks for dynamic LDS beyond the kernel's own tiles so that a workgroup holds
+// more than half of a compute unit's LDS: then at most one workgroup (of this
+// or any other such launch) runs per compute unit.  Fewer waves streaming at
+// once keep fewer DRAM rows open at a time; on the 1.1B-parameter workload
+// two waves per compute unit moved the stage from 5.5 to 6.1 TB/s.
+template <int R, bool BF16, int G, bool NORM, int WAVES>
+void launch_per_worker_waves(bool one_per_cu, const void* grad, float* h, const float* g,
+                             const float* V, const RowGroup* groups, int64_t ngroups, float* S,
+                             int64_t d, int64_t m, int32_t N, float eta, float a,
+                             hipStream_t stream) {
+  constexpr size_t kStatic = (size_t)WAVES * wave_lds_f4<R, G, NORM>() * sizeof(float4);
+  constexpr size_t kHalf = kLdsPerCu / 2 + 1024;  // a margin past one half
+  static_assert(kStatic < kHalf, "the reservation below assumes tiles under half the LDS");
+  const size_t reserve = one_per_cu ? kHalf - kStatic : 0;
+  hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16, G, WAVES, NORM>),
+                     dim3(blocks_for(ngroups, WAVES), (unsigned)N), dim3(WAVES * kWave),
+                     reserve, stream, grad, h, g, V, groups, ngroups, S, d, m, eta, a);
+}
+
+template <int R, bool BF16, int G, bool NORM>
+void launch_per_worker(const SketchOccupancy& occ, const void* grad, float* h, const float* g,
+                       const float* V, const RowGroup* groups, int64_t ngroups, float* S,
+                       int64_t d, int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
+  if (occ.waves == 2)
+    launch_per_worker_waves<R, BF16, G, NORM, 2>(occ.one_per_cu != 0, grad, h, g, V, groups,
+                                                 ngroups, S, d, m, N, eta, a, stream);
+  else
+    launch_per_worker_waves<R, BF16, G, NORM, 4>(occ.one_per_cu != 0, grad, h, g, V, groups,
+                                                 ngroups, S, d, m, N, eta, a, stream);
 }
 
 // Worker sum P = S^(0) + S^(1) + ... (ascending worker order) and importance
@@ -347,13 +377,11 @@ reduce_rows_kernel(const float* __restrict__ S, float* __restrict__ sigma, int64
 
 template <int R, bool BF16, int G>
 struct PerWorkerLaunch {
-  static void run(const void* grad, float* h, const float* g, const float* V,
-                  const RowGroup* groups, int64_t ngroups, float* S, int64_t d, int64_t m,
-                  int32_t N, float eta, float a, hipStream_t stream) {
-    hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16, G>),
-                       dim3(blocks_for(ngroups, kSketchWaves), (unsigned)N),
-                       dim3(kSketchWaves * kWave), 0, stream, grad, h, g, V, groups,
-                       ngroups, S, d, m, eta, a);
+  static void run(const SketchOccupancy& occ, const void* grad, float* h, const float* g,
+                  const float* V, const RowGroup* groups, int64_t ngroups, float* S, int64_t d,
+                  int64_t m, int32_t N, float eta, float a, hipStream_t stream) {
+    launch_per_worker<R, BF16, G, false>(occ, grad, h, g, V, groups, ngroups, S, d, m, N, eta,
+                                         a, stream);
   }
 };
 
@@ -391,9 +419,9 @@ hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_
                                     float* h, const float* g, const float* V,
                                     const RowGroup* groups, int64_t ngroups, float* S,
                                     int64_t d, int64_t m, int32_t N, int32_t r, float eta,
-                                    float a, hipStream_t stream) {
+                                    float a, SketchOccupancy occ, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
-  if (!dispatch<PerWorkerLaunch>(r, grad_bf16 != 0, group_rows, grad, h, g, V, groups,
+  if (!dispatch<PerWorkerLaunch>(r, grad_bf16 != 0, group_rows, occ, grad, h, g, V, groups,
                                  ngroups, S, d, m, N, eta, a, stream))
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -402,17 +430,16 @@ hipError_t launch_sketch_per_worker(int32_t group_rows, const void* grad, int32_
 hipError_t launch_row_norms(int32_t group_rows, const void* grad, int32_t grad_bf16, float* h,
                             const float* g, const float* V, const RowGroup* groups, int64_t ngroups,
                             float* norms, int64_t d, int64_t m, int32_t N, float eta, float a,
-                            hipStream_t stream) {
+                            SketchOccupancy occ, hipStream_t stream) {
   if (ngroups <= 0) return hipSuccess;
-  const dim3 grid(blocks_for(ngroups, kSketchWaves), (unsigned)N), block(kSketchWaves * kWave);
 #define ARC_NORM_CASE(GG)                                                                    \
   case GG:                                                                                   \
     if (grad_bf16)                                                                           \
-      hipLaunchKernelGGL((sketch_per_worker_kernel<1, true, GG, true>), grid, block, 0,      \
-                         stream, grad, h, g, V, groups, ngroups, norms, d, m, eta, a);       \
+      launch_per_worker<1, true, GG, true>(occ, grad, h, g, V, groups, ngroups, norms, d, m, \
+                                           N, eta, a, stream);                               \
     else                                                                                     \
-      hipLaunchKernelGGL((sketch_per_worker_kernel<1, false, GG, true>), grid, block, 0,     \
-                         stream, grad, h, g, V, groups, ngroups, norms, d, m, eta, a);       \
+      launch_per_worker<1, false, GG, true>(occ, grad, h, g, V, groups, ngroups, norms, d,   \
+                                            m, N, eta, a, stream);                           \
     break;
   switch (group_rows) {
     ARC_NORM_CASE(64)

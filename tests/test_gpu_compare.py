@@ -75,6 +75,7 @@ CASES = [
     ("tensors_bf16", dict(d=sum(a * b for a, b, _ in MIXED), N=2, tensors=MIXED,
                           grad_dtype="bf16", family=1)),
     ("partial_chunks_per_worker", dict(d=1000 * 60 + 996, N=5, n=1000, K=7)),
+    ("two_wave_rows", dict(d=2304 * 120 + 36, N=3, n=2304, K=5, grad_dtype="bf16", family=1)),
     ("tensors_partial_bf16", dict(d=sum(a * b for a, b, _ in PARTIAL), N=3, tensors=PARTIAL,
                                   grad_dtype="bf16", family=1)),
 ]

@@ -79,6 +79,15 @@ CASES = [
                                                grad_dtype="bf16", family=1)),
     ("partial_chunk_n4_per_worker", dict(d=4 * 5000, N=5, n=4, r=2, K=60, steps=2)),
     ("ragged_tail_r1_per_worker", dict(d=512 * 300 + 12, N=6, n=512, r=1, K=9, steps=2)),
+    # rows of 9 or more chunks: workgroups of two waves, one per compute unit
+    # (8-, 16-, 32- and 64-row groups, a partial last chunk, a ragged tail row)
+    ("two_wave_g8_bf16", dict(d=2304 * 150 + 100, N=3, n=2304, r=4, K=7, steps=2,
+                              grad_dtype="bf16", family=1)),
+    ("two_wave_g16_bf16_N4", dict(d=2048 * 120, N=4, n=2048, r=4, K=6, steps=2,
+                                  grad_dtype="bf16", family=1)),
+    ("two_wave_g32_r2", dict(d=576 * 500, N=2, n=576, r=2, K=9, steps=2)),
+    ("two_wave_g64_r8", dict(d=288 * 700 + 4, N=2, n=288, r=8, K=12, steps=2)),
+    ("two_wave_partial_r1_N5", dict(d=2308 * 100 + 8, N=5, n=2308, r=1, K=4, steps=2)),
 ]
 
 
@@ -104,6 +113,16 @@ def test_describe_names_the_kernel_path():
         assert "sketch=general" in comp.describe()
     finally:
         comp.close()
+    # launch shapes: one 256-column chunk per row runs uncapped, 3 chunks in
+    # 4-wave workgroups and 16 chunks in 2-wave ones, one per compute unit
+    for n, want in ((256, "workgroup_waves=(4 4 4 4)"), (768, "workgroup_waves=(4 4 4 4/cu)"),
+                    (2048, "workgroup_waves=(4 4 2/cu 4)")):
+        comp = arc.Compressor(d=n * 64, N=2, n=n, r=4, K=3, eta=0.1, seed=1)
+        try:
+            desc = comp.describe()
+            assert want in desc, desc
+        finally:
+            comp.close()
     # a width that is a multiple of 4 but of no chunk width, with a ragged
     # tail row: all vector groups, no general kernel
     comp = arc.Compressor(d=100 * 64 + 8, N=2, n=100, r=4, K=3, eta=0.1, seed=1)

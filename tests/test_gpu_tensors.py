@@ -39,6 +39,12 @@ MIXED = [(70, 147, 9), (3, 33, 1), (64, 96, 5), (1, 7, 1), (129, 64, 4), (1, 64,
 PARTIAL = [(70, 100, 9), (1, 1000, 1), (33, 36, 3), (5, 4, 2), (129, 200, 4), (2, 520, 1),
            (64, 96, 5), (300, 44, 11)]
 
+# Wide rows: 16-row groups of 2048 columns and 32-row groups of 576 (16 and 9
+# chunks) take workgroups of two waves, one per compute unit, while the
+# 8-row groups (768, 3072 and 4096 columns: 8.1 chunks on average) take
+# workgroups of four, one per compute unit, in a launch beside them.
+WIDE = [(40, 2048, 3), (100, 768, 5), (30, 3072, 2), (1, 4096, 1), (64, 576, 4)]
+
 
 def _random_layout(seed, count, max_rows=300):
     rng = np.random.default_rng(seed)
@@ -74,6 +80,8 @@ CASES = [
                                         family=1)),
     ("partial_r8_N2", dict(tensors=PARTIAL, N=2, r=8, steps=2)),
     ("partial_r1_bf16_N7", dict(tensors=PARTIAL, N=7, r=1, steps=2, grad_dtype="bf16", family=1)),
+    ("wide_two_wave_bf16_N3", dict(tensors=WIDE, N=3, r=4, steps=2, grad_dtype="bf16", family=1)),
+    ("wide_two_wave_r1_N2", dict(tensors=WIDE, N=2, r=1, steps=2)),
     ("one_tensor_multiblock_select", dict(tensors=[(40_000, 32, 9_000)], N=2, r=4, steps=2)),
     ("single_one_row_tensor", dict(tensors=[(1, 4096, 1)], N=2, r=4, steps=2)),
     ("all_k_zero", dict(tensors=[(64, 64, 0), (10, 32, 0)], N=2, r=4, steps=2)),
@@ -103,6 +111,15 @@ def test_tensor_parity_zero_residual_ties():
     log("[tensors] zero residual")
     run_case(label="tensors_zeros", d=d, N=2, r=4, tensors=ALIGNED, steps=2,
              grad_fn=lambda t: zero)
+
+
+def test_tensor_mode_launch_shapes():
+    comp = arc.Compressor(d=_d(WIDE), N=2, r=4, tensors=WIDE, eta=0.1, seed=1)
+    try:
+        desc = comp.describe()
+        assert "workgroup_waves=(4 2/cu 2/cu 4/cu)" in desc, desc
+    finally:
+        comp.close()
 
 
 def test_tensor_mode_describe_and_payload():
