@@ -183,9 +183,10 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  * background for the next call) and waits until the device has read the
  * projection staged two calls earlier, so it cannot be captured into a HIP
  * graph.
- * The streaming kernel's workgroups on rows of two or more chunks each hold
- * just over half of a compute unit's LDS (one workgroup per compute unit):
- * while it runs, another kernel's workgroups that need more than the
+ * On rows longer than the streaming kernel's column chunk (32 to 256
+ * values, by how many rows it streams together), its workgroups each hold
+ * just over half of a compute unit's LDS, so that one runs per compute
+ * unit: while it runs, another kernel's workgroups that need more than the
  * remaining LDS wait for a compute unit to free up.
  */
 arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
