@@ -266,6 +266,9 @@ def main():
               "(workers are simulated on the device); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
+
     import torch
 
     if args.copy_calibration > 0:
@@ -326,10 +329,19 @@ def main():
         stream.synchronize()
         stage_ms, nsteps = arc.arc_timing_read(comp.ctx)
         arc.arc_timing_enable(comp.ctx, False)
+        # The spread of single steps: as many steps again, an event after each.
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        evs[0].record(stream)
+        for k in range(args.steps):
+            t = args.warmup + 2 * args.steps + k
+            comp.step(t, grads[t % nb], h, g)
+            evs[k + 1].record(stream)
+        evs[-1].synchronize()
+        per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
         model = None
         if not args.no_model_step and args.compressor != "topk":
             model = model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb,
-                                      args.warmup + 2 * args.steps)
+                                      args.warmup + 3 * args.steps)
     ms_per_step = total_ms / args.steps
     stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
     log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
@@ -376,6 +388,10 @@ def main():
                    "compressor": args.compressor,
                    "tensors": len(w.views) if w.per_tensor else 0,
                    "payload_elems": comp.payload},
+        "step_ms_spread": {"median": per_step[len(per_step) // 2] if len(per_step) % 2
+                           else 0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2]),
+                           "min": per_step[0], "max": per_step[-1], "steps": len(per_step),
+                           "how": "a separate pass of as many steps, an event after each"},
         "step_hbm_GBps": step_gbps,
         "step_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "stage_ms": stages,
