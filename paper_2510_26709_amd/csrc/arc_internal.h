@@ -52,9 +52,11 @@ struct BucketState {
   int64_t kleft;
 };
 
-// A group of up to 64 consecutive rows of one view (one wave's rows in the
-// sketch kernels; the vectorised kernels take groups of 64, 32 or 16 rows).  Rows are `cols` wide and start `elem_off` coordinates into
-// each worker's vector; their projection is V[v_off .. v_off + cols*r).
+// A group of up to 64 rows of one view, `stride` rows apart (one wave's rows
+// in the sketch kernels; the vectorised kernels take groups of 64, 32, 16 or
+// 8 rows).  Rows are `cols` wide; local row l starts elem_off + l*stride*cols
+// coordinates into each worker's vector and is global row row0 + l*stride;
+// their projection is V[v_off .. v_off + cols*r).
 struct RowGroup {
   int64_t elem_off;  // coordinate of the group's first element
   int64_t row0;      // global index of the group's first row
@@ -62,7 +64,7 @@ struct RowGroup {
   int32_t rows;      // 1..64
   int32_t cols;      // row width
   int32_t last_len;  // valid columns of the last row (< cols for a ragged tail)
-  int32_t pad;
+  int32_t stride;    // rows between local rows: 1, or more in vectorised groups
 };
 
 // One tensor (selection bucket) of the per-tensor mode, for the gather.

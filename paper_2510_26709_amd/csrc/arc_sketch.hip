@@ -55,19 +55,22 @@ constexpr int slice_f4() {
 template <int R, int G, bool NORM>
 constexpr int wave_lds_f4() { return kTileF4 + slice_f4<R, G, NORM>(); }
 // Offset whose access the hardware drops: a group spans at most 2^30 bytes
-// (64 rows of at most 2^22 binary32 values), so 2^31, and the 2^30 it becomes
-// for the bf16 stream's halved offsets, lie beyond every resource here.
+// (64 consecutive rows of at most 2^22 binary32 values; the host keeps
+// groups of rows further apart within the same span), so 2^31, and the 2^30
+// it becomes for the bf16 stream's halved offsets, lie beyond every
+// resource here.
 constexpr uint32_t kDropOffset = 0x80000000u;
 
 // One wave's pass over the rows of one row group of worker i: loads the
 // grad/h/g tile of each chunk with coalesced 16-byte accesses, applies (11a),
 // writes h back, parks Delta in LDS, then runs this lane's r chains over its
-// row.  Local row l of the group starts at coordinate elem_off + l*n; n is a
-// multiple of 4 but need not be one of the chunk width, in which case each
-// row's last chunk is partial: its lanes past the row's end load and store
-// nothing, and the chains stop at the row's end.  The three streams are read
-// through buffer resources that end at the group's last row, so in a group
-// of fewer than G rows the missing rows read as zero and are not stored.
+// row.  Local row l of the group starts at coordinate elem_off + l*stride*n;
+// n is a multiple of 4 but need not be one of the chunk width, in which case
+// each row's last chunk is partial: its lanes past the row's end load and
+// store nothing, and the chains stop at the row's end.  The three streams are
+// read through buffer resources that end at the group's last row, so in a
+// group of fewer than G rows (always consecutive rows, stride 1) the missing
+// rows read as zero and are not stored.
 // Lanes G..63 repeat the chains of lanes 0..G-1; the caller keeps only lanes
 // below the group's row count.  NORM (R = 1): the chain is the row's squared
 // norm, fmaf(Delta, Delta, s), and V is unused.
@@ -90,8 +93,9 @@ __device__ __forceinline__ void sketch_rows(
   const int quad = lane % kLPR;  // 16-byte column group within the chunk
   const uint32_t n = (uint32_t)grp.cols;
   const int32_t rows = grp.rows;
+  const uint32_t rstride = (uint32_t)grp.stride;
   const int64_t wbase = (int64_t)i * d + grp.elem_off;
-  const uint32_t bytes = (uint32_t)rows * n * 4u;
+  const uint32_t bytes = ((uint32_t)(rows - 1) * rstride + 1u) * n * 4u;
   const buffer_rsrc rh = make_buffer(h + wbase, bytes);
   const buffer_rsrc rg = make_buffer(g + wbase, bytes);
   const buffer_rsrc rx =
@@ -101,7 +105,7 @@ __device__ __forceinline__ void sketch_rows(
   // byte offset of this lane's 16 bytes of binary32 in row u*kRPL + sub
   uint32_t off[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * kRPL + sub) * n + quad * 4) * 4u;
+  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * kRPL + sub) * rstride * n + quad * 4) * 4u;
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
   float s_own = 0.0f;  // (row, k) lanes: this lane's chain
@@ -301,7 +305,7 @@ sketch_per_worker_kernel(const void* __restrict__ grad, float* __restrict__ h,
   float s[R];
   sketch_rows<R, BF16, G, NORM>(grad, h, g, V, d, grp, i, eta, a, tiles[wave], s);
   if (lane < grp.rows) {
-    float* out = S + ((int64_t)i * m + grp.row0 + lane) * R;
+    float* out = S + ((int64_t)i * m + grp.row0 + (int64_t)lane * grp.stride) * R;
 #pragma unroll
     for (int k = 0; k < R; ++k) out[k] = s[k];
   }

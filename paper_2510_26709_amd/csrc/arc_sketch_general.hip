@@ -3,7 +3,9 @@
 // for row groups the 16-byte kernels cannot take: any row width, any r up to
 // ARC_MAX_R, element-aligned pointers, and a ragged last row.
 //
-// One wave per (row group, worker).  Each 32-column chunk of the group's
+// One wave per (row group, worker); a group's rows may lie `stride` rows
+// apart (vectorised groups, taken here when the pointers are misaligned).
+// Each 32-column chunk of the group's
 // 64 x 32 tile is loaded with one element per lane (two rows of 32 columns
 // per instruction, coalesced), 24 loads in flight per pass of 16 rows; Delta
 // goes to LDS, and so do the chunk's 32 rows of V (transposed to [k][j]).
@@ -42,6 +44,7 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
   const int32_t i = blockIdx.y;
   const int64_t n = grp.cols;
   const int32_t rows = grp.rows;
+  const int64_t row_step = (int64_t)grp.stride * n;  // elements between local rows
   const int64_t base = (int64_t)i * d + grp.elem_off;
   const float* Vg = V + grp.v_off;
   const int half = lane >> 5;            // row of the pair this lane loads
@@ -69,7 +72,7 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
         const int l = pass * kGenRowsPerPass + u * 2 + half;
         const int64_t len = l == rows - 1 ? grp.last_len : n;
         ok[u] = l < rows && cl < cw && c0 + cl < len;
-        e[u] = ok[u] ? base + (int64_t)l * n + c0 + cl : base;
+        e[u] = ok[u] ? base + (int64_t)l * row_step + c0 + cl : base;
         if constexpr (BF16)
           xv[u] = __uint_as_float((uint32_t)static_cast<const uint16_t*>(grad)[e[u]] << 16);
         else
@@ -111,7 +114,7 @@ sketch_general_kernel(const void* __restrict__ grad, float* __restrict__ h,
     wave_lds_fence();
   }
   if (lane < rows) {
-    float* out = S + ((int64_t)i * m + grp.row0 + lane) * r;
+    float* out = S + ((int64_t)i * m + grp.row0 + (int64_t)lane * grp.stride) * r;
     for (int32_t k = 0; k < r; ++k) out[k] = acc[k * kWave + lane];
   }
 }

@@ -115,12 +115,15 @@ def test_describe_names_the_kernel_path():
         comp.close()
     # launch shapes: one 256-column chunk per row runs uncapped, 3 chunks in
     # 4-wave workgroups and 16 chunks in 2-wave ones, one per compute unit
-    for n, want in ((256, "workgroup_waves=(4 4 4 4)"), (768, "workgroup_waves=(4 4 4 4/cu)"),
-                    (2048, "workgroup_waves=(4 4 2/cu 4)")):
-        comp = arc.Compressor(d=n * 64, N=2, n=n, r=4, K=3, eta=0.1, seed=1)
+    # and 16-chunk rows in groups of every 4th row of a block of 4 groups
+    for n, want, strided in ((256, "workgroup_waves=(4 4 4 4)", 0),
+                             (768, "workgroup_waves=(4 4 4 4/cu)", 0),
+                             (2048, "workgroup_waves=(4 4 2/cu 4)", 4)):
+        comp = arc.Compressor(d=n * 70, N=2, n=n, r=4, K=3, eta=0.1, seed=1)
         try:
             desc = comp.describe()
             assert want in desc, desc
+            assert f"interleaved_groups={strided} " in desc, desc
         finally:
             comp.close()
     # a width that is a multiple of 4 but of no chunk width, with a ragged
@@ -145,9 +148,12 @@ def test_parity_steps_out_of_order():
 TENSORS_3W = [(300, 64, 5), (40, 1000, 3), (129, 256, 4), (1, 2048, 1)]
 
 
-def test_parity_misaligned_pointers_take_the_general_path():
-    log("[parity] misaligned")
-    run_case(label="misaligned", d=256 * 120, N=3, n=256, r=4, K=11, steps=2, misalign=1)
+@pytest.mark.parametrize("n,rows", [(256, 120), (2304, 70)])
+def test_parity_misaligned_pointers_take_the_general_path(n, rows):
+    # 2304-wide rows: the vectorised plan's groups take every 4th row of a
+    # block of 32, and the general kernel must follow them
+    log(f"[parity] misaligned n={n}")
+    run_case(label=f"misaligned_{n}", d=n * rows, N=3, n=n, r=4, K=11, steps=2, misalign=1)
 
 
 def test_parity_buckets():

@@ -41,9 +41,11 @@ PARTIAL = [(70, 100, 9), (1, 1000, 1), (33, 36, 3), (5, 4, 2), (129, 200, 4), (2
 
 # Wide rows: 16-row groups of 2048 columns and 32-row groups of 576 (16 and 9
 # chunks) take workgroups of two waves, one per compute unit, while the
-# 8-row groups (768, 3072 and 4096 columns: 8.1 chunks on average) take
-# workgroups of four, one per compute unit, in a launch beside them.
-WIDE = [(40, 2048, 3), (100, 768, 5), (30, 3072, 2), (1, 4096, 1), (64, 576, 4)]
+# 8-row groups (768, 3072 and 4096 columns: 8.7 chunks on average) take
+# workgroups of four, one per compute unit, in a launch beside them.  The
+# first 64 rows of the 2048-wide tensor and the first 32 of the 3072-wide
+# one form groups of every 4th row.
+WIDE = [(70, 2048, 3), (100, 768, 5), (40, 3072, 2), (1, 4096, 1), (64, 576, 4)]
 
 
 def _random_layout(seed, count, max_rows=300):
@@ -117,7 +119,7 @@ def test_tensor_mode_launch_shapes():
     comp = arc.Compressor(d=_d(WIDE), N=2, r=4, tensors=WIDE, eta=0.1, seed=1)
     try:
         desc = comp.describe()
-        assert "workgroup_waves=(4 2/cu 2/cu 4/cu)" in desc, desc
+        assert "workgroup_waves=(4 2/cu 2/cu 4/cu) interleaved_groups=8 " in desc, desc
     finally:
         comp.close()
 
