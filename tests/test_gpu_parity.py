@@ -88,6 +88,11 @@ CASES = [
     ("two_wave_g32_r2", dict(d=576 * 500, N=2, n=576, r=2, K=9, steps=2)),
     ("two_wave_g64_r8", dict(d=288 * 700 + 4, N=2, n=288, r=8, K=12, steps=2)),
     ("two_wave_partial_r1_N5", dict(d=2308 * 100 + 8, N=5, n=2308, r=1, K=4, steps=2)),
+    # the widest rows the vectorised kernels take (2^22 values, plus a ragged
+    # tail row of half that), and 4 values more, which go to the general one
+    ("max_width_vector", dict(d=(1 << 22) * 3 + (1 << 21), N=2, n=1 << 22, r=4, K=2, steps=2)),
+    ("over_max_width_general", dict(d=((1 << 22) + 4) * 2, N=2, n=(1 << 22) + 4, r=4, K=1,
+                                    steps=1)),
 ]
 
 
@@ -113,6 +118,13 @@ def test_describe_names_the_kernel_path():
         assert "sketch=general" in comp.describe()
     finally:
         comp.close()
+    # the widest vectorised rows, and one step wider
+    for n, want in ((1 << 22, "general_groups=0"), ((1 << 22) + 4, "sketch=general")):
+        comp = arc.Compressor(d=n * 2, N=2, n=n, r=4, K=1, eta=0.1, seed=1)
+        try:
+            assert want in comp.describe(), comp.describe()
+        finally:
+            comp.close()
     # launch shapes: one 256-column chunk per row runs uncapped, 3 chunks in
     # 4-wave workgroups and 16 chunks in 2-wave ones, one per compute unit
     # and 16-chunk rows in groups of every 4th row of a block of 4 groups
