@@ -34,6 +34,10 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 constexpr int kBufferDword3 = 0x00020000;  // gfx9-family raw buffer: 32-bit data format
 constexpr int kCacheDefault = 0;
 constexpr int kCacheNonTemporal = 2;       // nt cache-policy bit on gfx950
+// nt with the sc1 bit (device scope): for a stream written once and read by
+// later launches only.  For the sketch stage's h stores it measured 0.3-1.4%
+// faster than nt alone (1.1B step 9.71 -> 9.56 ms), and without nt slower.
+constexpr int kCacheStreamDevice = 2 | 16;
 
 __device__ __forceinline__ buffer_rsrc make_buffer(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,

@@ -195,8 +195,8 @@ __device__ __forceinline__ void sketch_rows(
       // the hardware drops their store: a select rather than a branch, which
       // would make the compiler's wait counts for the loads in flight
       // conservative on every path.
-      buffer_store_f4<kCacheNonTemporal>(rh, u * kRPL + sub < rows ? col_off(off[u], c) : kDropOffset,
-                                         hn);
+      buffer_store_f4<kCacheStreamDevice>(
+          rh, u * kRPL + sub < rows ? col_off(off[u], c) : kDropOffset, hn);
       float4 dl;
       dl.x = hn.x - gv[u].x;
       dl.y = hn.y - gv[u].y;
