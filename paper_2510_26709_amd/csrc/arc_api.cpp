@@ -72,16 +72,16 @@ bool vector_r(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8; }
 // 0.38 -> 0.35 ms, per-tensor ResNet-18 0.54 -> 0.51 ms, GPT-2 small
 // 3.06 -> 3.00 ms (per tensor 3.23 -> 3.17), TinyLlama 11.87 -> 11.60 ms
 // (per tensor 12.02 -> 11.70).
-// One measured exception: rows of exactly 2048 values stream faster in
-// 16-row groups (128-column chunks) than in 8-row ones (1.1B workload 11.10
-// vs 11.39 ms; binary32 gradients at that width 5.56 vs 5.77 ms), while at
-// 768, 1024 and 3072 values 8-row groups are 2-5% faster and at 4096 and
-// 5632 the two tie.
+// The exception: power-of-two widths from 1024 to 4096 take 16-row groups,
+// which with the launch shapes and row spacing below stream 4-9% faster
+// than 8-row groups do with theirs (step ms for 1.1·10⁹ bf16 elements, 4
+// workers: 1024 values 2.39 vs 2.57, 2048 2.44 vs 2.67, 4096 2.51 vs 2.60);
+// at 8192 the two tie and at 16384 8-row groups are 17% faster.
 constexpr int32_t kGroupSizes[] = {8, 16, 32, 64};
-constexpr int64_t kSixteenRowWidth = 2048;
+bool power_of_two(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 int32_t vector_group_rows(int64_t cols) {
   if (cols > (int64_t{1} << 22) || cols % 4 != 0) return 0;
-  if (cols == kSixteenRowWidth) return 16;
+  if (power_of_two(cols) && cols >= 1024 && cols <= 4096) return 16;
   for (int32_t gr : kGroupSizes)
     if (cols % arc::vector_chunk_cols(gr) == 0) return gr;
   for (int32_t gr : kGroupSizes)
@@ -314,8 +314,11 @@ int size_slot(int32_t group_rows) {
 // / 10.09; 4096-wide in 8-row groups (16 chunks) 33.97 / 32.03 / 31.15;
 // 768-wide in 8-row groups (3 chunks) 2.88 / 2.76 / 2.93; 512-wide (2
 // chunks) 0.350 / 0.345 / 0.370; 256-wide (one chunk, a 50 MB working set)
-// 0.047 / 0.049 / 0.053.
-constexpr double kTwoWaveChunks = 9.0;
+// 0.047 / 0.049 / 0.053.  16-row groups, whose chunks are half as wide,
+// gain from 2 waves from 6 chunks on (768 values: 2.73 vs 2.78 ms; 1024:
+// 2.42 vs 2.49 ms at 1.1·10⁹ elements), 8-row groups from 9 (2048 values:
+// 10.67 vs 10.39 ms on the 1.1B workload, 2304: 2.82 vs 2.89 ms).
+int32_t two_wave_chunks(int32_t group_rows) { return group_rows == 16 ? 6 : 9; }
 arc::SketchOccupancy sketch_occupancy(const std::vector<arc::RowGroup>& groups,
                                       int32_t group_rows) {
   double elems = 0.0, weighted = 0.0;
@@ -326,26 +329,31 @@ arc::SketchOccupancy sketch_occupancy(const std::vector<arc::RowGroup>& groups,
     weighted += e * static_cast<double>((grp.cols + cw - 1) / cw);
   }
   const double chunks = elems > 0.0 ? weighted / elems : 0.0;
-  if (chunks >= kTwoWaveChunks) return {2, 1};
+  if (chunks >= two_wave_chunks(group_rows)) return {2, 1};
   if (chunks >= 2.0) return {4, 1};
   return {4, 0};
 }
 
 // Rows between the local rows of a full vectorised group.  A wave streams
-// its rows a chunk at a time, one short run per row; with its rows 4 apart,
-// the runs of the 4 groups of a block (next to each other in the launch)
-// interleave in memory.  Measured (step ms, rows 1 / 2 / 4 / 8 apart):
-// 1.1B (2048-wide, 16 chunks) 10.11 / 9.82 / 9.68 / 10.87; per-tensor 1.1B
-// 10.67 / 10.41 / 10.27 / 11.20; 7B (4096-wide) 31.42 / 31.35 / 31.42 /
-// 32.52; GPT-2 small (3 chunks) 2.77 for all; ResNet-18 (2 chunks) 0.349 /
-// 0.352 / 0.357 / 0.355.  So rows of fewer than kTwoWaveChunks chunks stay
-// consecutive.  Strided groups span at most 2^30 bytes.
+// its rows a chunk at a time, one short run per row; with its rows S apart,
+// the runs of the S groups of a block (next to each other in the launch)
+// interleave in memory.  Power-of-two widths do best with a group's rows
+// 32 KiB apart (S = 8192 / width, 1 from 8192 on: step ms for 1.1·10⁹ bf16
+// elements, 4 workers, rows 1 / 2 / 4 / 8 apart: 1024 values 2.60 / 2.48 /
+// 2.42 / 2.39; 2048 2.54 / 2.47 / 2.44 / -; 4096 2.55 / 2.51 / 2.89 / 2.87;
+// 8192 with 8-row groups 2.51 / 2.55 / 2.79 / 2.80).  Other widths take rows
+// 4 apart (3072 values 2.77 vs 2.70 ms; 2304 and 5632 unchanged).  Rows of
+// too few chunks for two waves stay consecutive (768 values: equal; 512: 1-2%
+// slower apart).  Strided groups span at most 2^30 bytes.
+constexpr int64_t kPowerOfTwoRowBytes = 32 * 1024;
 constexpr int32_t kRowInterleave = 4;
 int32_t row_interleave(int64_t cols, int32_t group_rows) {
   const int64_t cw = arc::vector_chunk_cols(group_rows);
-  if (static_cast<double>((cols + cw - 1) / cw) < kTwoWaveChunks) return 1;
-  const int64_t span = ((group_rows - 1) * int64_t{kRowInterleave} + 1) * cols * 4;
-  return span <= (int64_t{1} << 30) ? kRowInterleave : 1;
+  if ((cols + cw - 1) / cw < two_wave_chunks(group_rows)) return 1;
+  int64_t S = kRowInterleave;
+  if (power_of_two(cols)) S = std::max<int64_t>(1, kPowerOfTwoRowBytes / (cols * 4));
+  const int64_t span = ((group_rows - 1) * S + 1) * cols * 4;
+  return span <= (int64_t{1} << 30) ? static_cast<int32_t>(S) : 1;
 }
 
 // Row groups over `rows` rows of width `cols` that start at coordinate

@@ -88,6 +88,12 @@ CASES = [
     ("two_wave_g32_r2", dict(d=576 * 500, N=2, n=576, r=2, K=9, steps=2)),
     ("two_wave_g64_r8", dict(d=288 * 700 + 4, N=2, n=288, r=8, K=12, steps=2)),
     ("two_wave_partial_r1_N5", dict(d=2308 * 100 + 8, N=5, n=2308, r=1, K=4, steps=2)),
+    # power-of-two widths in 16-row groups with rows 8 and 2 apart, and a
+    # 7-chunk width in 16-row groups of 2 waves with rows 4 apart
+    ("pow2_1024_rows8apart", dict(d=1024 * 300 + 4, N=3, n=1024, r=4, K=5, steps=2)),
+    ("pow2_4096_rows2apart_bf16", dict(d=4096 * 80, N=2, n=4096, r=4, K=3, steps=2,
+                                        grad_dtype="bf16", family=1)),
+    ("g16_896_two_wave_r2", dict(d=896 * 150, N=3, n=896, r=2, K=6, steps=2)),
     # the widest rows the vectorised kernels take (2^22 values, plus a ragged
     # tail row of half that), and 4 values more, which go to the general one
     ("max_width_vector", dict(d=(1 << 22) * 3 + (1 << 21), N=2, n=1 << 22, r=4, K=2, steps=2)),
@@ -127,11 +133,14 @@ def test_describe_names_the_kernel_path():
             comp.close()
     # launch shapes: one 256-column chunk per row runs uncapped, 3 chunks in
     # 4-wave workgroups and 16 chunks in 2-wave ones, one per compute unit
-    # and 16-chunk rows in groups of every 4th row of a block of 4 groups
-    for n, want, strided in ((256, "workgroup_waves=(4 4 4 4)", 0),
-                             (768, "workgroup_waves=(4 4 4 4/cu)", 0),
-                             (2048, "workgroup_waves=(4 4 2/cu 4)", 4)):
-        comp = arc.Compressor(d=n * 70, N=2, n=n, r=4, K=3, eta=0.1, seed=1)
+    # and 16-chunk rows in groups of every 4th row of a block of 4 groups;
+    # power-of-two widths from 1024 take 16-row groups whose rows lie 32 KiB
+    # apart (8 rows apart at 1024 values)
+    for n, rows, want, strided in ((256, 70, "workgroup_waves=(4 4 4 4)", 0),
+                                   (768, 70, "workgroup_waves=(4 4 4 4/cu)", 0),
+                                   (2048, 70, "workgroup_waves=(4 4 2/cu 4)", 4),
+                                   (1024, 140, "workgroup_waves=(4 4 2/cu 4)", 8)):
+        comp = arc.Compressor(d=n * rows, N=2, n=n, r=4, K=3, eta=0.1, seed=1)
         try:
             desc = comp.describe()
             assert want in desc, desc
