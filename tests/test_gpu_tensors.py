@@ -105,6 +105,10 @@ def test_tensor_parity_misaligned_pointers():
     log("[tensors] misaligned")
     run_case(label="tensors_misaligned", d=_d(ALIGNED), N=3, r=4, tensors=ALIGNED, steps=2,
              misalign=1, check_S=True)
+    # groups of rows 4 apart, taken by the general kernel
+    log("[tensors] misaligned wide")
+    run_case(label="tensors_misaligned_wide", d=_d(WIDE), N=2, r=4, tensors=WIDE, steps=1,
+             misalign=1, check_S=True)
 
 
 def test_tensor_parity_zero_residual_ties():
