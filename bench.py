@@ -125,14 +125,24 @@ def _prefix(w, elems):
     return d_s, dict(tensors=take), f"first {len(take)} of {len(views)} tensors (K={K_s} rows)"
 
 
-def cpu_baseline(w, grads_dev, seconds_target=12.0):
+def cpu_baseline(w, grads_dev, seconds_target=12.0, threads=0):
     """Time the CPU oracle on a prefix of the workload (the first coordinates
     of every worker's vector, whole rows or whole tensors) from h = g = 0, on
-    the same synthetic gradients (copied from the device)."""
+    the same synthetic gradients (copied from the device); threads > 0 limits
+    the oracle's thread count for this run."""
     import numpy as np
 
     import oracle
-    threads = oracle.num_threads()
+    all_threads = oracle.num_threads()
+    if threads > 0:
+        oracle.set_num_threads(threads)
+    try:
+        return _cpu_baseline(np, oracle, w, grads_dev, seconds_target, oracle.num_threads())
+    finally:
+        oracle.set_num_threads(all_threads)
+
+
+def _cpu_baseline(np, oracle, w, grads_dev, seconds_target, threads):
 
     def run(elems, steps=None, budget=None):
         """Oracle steps on the first `elems` coordinates: `steps` of them, or
@@ -366,6 +376,11 @@ def main():
         log("[bench] cpu baseline (oracle) ...")
         cpu = cpu_baseline(w, grads)
         log(f"[bench] cpu baseline {cpu['value']:.3e} elements/s on {cpu['cores']} threads")
+        if w.name == "tiny":
+            # the smallest workload is also reported on one thread
+            one = cpu_baseline(w, grads, seconds_target=6.0, threads=1)
+            cpu["single_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
+            log(f"[bench] cpu baseline {one['value']:.3e} elements/s on 1 thread")
     comp.close()
 
     out = {

@@ -62,6 +62,7 @@ def _load():
         "oracle_step_topk_tensors": (ctypes.c_int, [_i32, _f32, _i32, _vp, _vp, _vp, _vp, _i32,
                                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "oracle_num_threads": (ctypes.c_int, []),
+        "oracle_set_num_threads": (None, [ctypes.c_int]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -104,6 +105,12 @@ def num_rows(d: int, n: int) -> int:
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (results do not
+    depend on the count: every row's arithmetic runs in a fixed order)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def splitmix64(seed: int, x: int) -> int:

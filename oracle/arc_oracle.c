@@ -30,6 +30,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of later parallel loops (n >= 1); results do not depend on it. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ---------------------------------------------------------------------------
  * Shared random seed -> Gaussian projection V.
  *

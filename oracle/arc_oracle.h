@@ -154,6 +154,7 @@ int oracle_step_topk_tensors(int32_t N, float eta, int32_t num_tensors, const in
 
 /* Number of threads the oracle's parallel loops use. */
 int oracle_num_threads(void);
+void oracle_set_num_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -307,6 +307,25 @@ def test_thread_count_invariance():
     assert res[0] == res[1]
 
 
+def test_set_num_threads_changes_only_the_thread_count():
+    before = oracle.num_threads()
+    rng = np.random.default_rng(5)
+    N, d = 2, 32 * 301
+    grad = rng.standard_normal((N, d)).astype(F32)
+    outs = []
+    try:
+        for threads in (1, max(2, before)):
+            oracle.set_num_threads(threads)
+            assert oracle.num_threads() == threads
+            h, g = np.zeros((N, d), F32), np.zeros((N, d), F32)
+            out = oracle.step(h, g, grad, n=32, r=4, eta=0.3, seed=2, t=1, K=7)
+            outs.append((out["idx"].tobytes(), out["agg"].tobytes(), h.tobytes(), g.tobytes()))
+    finally:
+        oracle.set_num_threads(before)
+    assert oracle.num_threads() == before
+    assert outs[0] == outs[1]
+
+
 def test_step_rejects_bad_config_before_touching_state():
     h = np.ones((2, 8), F32)
     g = np.zeros((2, 8), F32)
