@@ -130,19 +130,21 @@ def cpu_baseline(w, grads_dev, seconds_target=12.0, threads=0):
     of every worker's vector, whole rows or whole tensors) from h = g = 0, on
     the same synthetic gradients (copied from the device); threads > 0 limits
     the oracle's thread count for this run."""
-    import numpy as np
-
     import oracle
     all_threads = oracle.num_threads()
     if threads > 0:
         oracle.set_num_threads(threads)
     try:
-        return _cpu_baseline(np, oracle, w, grads_dev, seconds_target, oracle.num_threads())
+        return _cpu_baseline(w, grads_dev, seconds_target)
     finally:
         oracle.set_num_threads(all_threads)
 
 
-def _cpu_baseline(np, oracle, w, grads_dev, seconds_target, threads):
+def _cpu_baseline(w, grads_dev, seconds_target):
+    import numpy as np
+
+    import oracle
+    threads = oracle.num_threads()
 
     def run(elems, steps=None, budget=None):
         """Oracle steps on the first `elems` coordinates: `steps` of them, or
