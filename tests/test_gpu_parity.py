@@ -283,3 +283,52 @@ def test_device_generator_matches_host_generator():
             dev_np = out.cpu().numpy().view(gen.np_dtype)
             host_np = gen.fill_host(t)
             assert dev_np.tobytes() == host_np.tobytes(), (kw, t)
+
+
+def test_two_contexts_on_two_streams_interleaved():
+    # Two compressors, each bound to its own stream (with its own side stream
+    # and projection staging), stepped alternately with no synchronisation in
+    # between: each must still match its own oracle run.
+    from parity_util import compare_float, to_device_grad
+
+    dev = torch.device("cuda:0")
+    cfgs = [dict(d=2304 * 70 + 100, N=3, n=2304, K=5, grad_dtype="bf16", family=1,
+                 data_seed=31, seed=5),
+            dict(d=768 * 300, N=2, n=768, K=7, grad_dtype="f32", family=0, data_seed=32,
+                 seed=6)]
+    steps = 3
+    streams = [torch.cuda.Stream(dev) for _ in cfgs]
+    comps, hs, gs, grads = [], [], [], []
+    try:
+        for c, s in zip(cfgs, streams):
+            comps.append(arc.Compressor(d=c["d"], N=c["N"], n=c["n"], r=4, K=c["K"], eta=0.1,
+                                        seed=c["seed"], grad_dtype=c["grad_dtype"], device=dev,
+                                        stream=s))
+            gen = synth.Generator(c["d"], c["N"], c["data_seed"], grad_dtype=c["grad_dtype"],
+                                  family=c["family"])
+            grads.append([gen.fill_host(t) for t in range(steps)])
+            hs.append(torch.zeros((c["N"], c["d"]), device=dev))
+            gs.append(torch.zeros((c["N"], c["d"]), device=dev))
+        dgrads = [[to_device_grad(x, dev) for x in gr] for gr in grads]
+        torch.cuda.synchronize(dev)
+        outs = [[], []]
+        for t in range(steps):
+            for k in range(2):
+                with torch.cuda.stream(streams[k]):
+                    idx, agg = comps[k].step(t, dgrads[k][t], hs[k], gs[k])
+                    outs[k].append((idx.clone(), agg.clone()))
+        torch.cuda.synchronize(dev)
+        for k, c in enumerate(cfgs):
+            log(f"[parity] two streams: context {k} {c}")
+            h_o = np.zeros((c["N"], c["d"]), F32)
+            g_o = np.zeros((c["N"], c["d"]), F32)
+            for t in range(steps):
+                want = oracle.step(h_o, g_o, grads[k][t], n=c["n"], r=4, eta=0.1, seed=c["seed"],
+                                   t=t, K=c["K"])
+                assert np.array_equal(outs[k][t][0].cpu().numpy(), want["idx"]), (k, t)
+                compare_float(f"ctx{k} t={t} agg", outs[k][t][1].cpu().numpy(), want["agg"])
+            compare_float(f"ctx{k} h", hs[k].cpu().numpy(), h_o)
+            compare_float(f"ctx{k} g", gs[k].cpu().numpy(), g_o)
+    finally:
+        for comp in comps:
+            comp.close()
