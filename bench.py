@@ -10,9 +10,14 @@ update.  Prints ONE JSON line:
   roofline     the streaming sketch kernel (the dominant one): algorithmic
                bytes per launch / its mean duration (HIP events on the
                library's stream over the timed region) against 8 TB/s
-  cpu_baseline the CPU oracle on a bounded prefix of the same workload
+  cpu_baseline the CPU oracle on a bounded prefix of the same workload, with
+               the threads it used, the host's core count and free memory
+  configs      the same report for further workloads timed in the same run
+               (by default GPT-2 small beside the 1.1B headline: the two
+               configurations the HBM-bandwidth target covers)
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--also NAME,...]
 """
 from __future__ import annotations
 
@@ -247,56 +252,28 @@ def copy_calibration(torch, gib, reps):
           flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--compressor", default="arc", choices=["arc", "randk", "topk"],
-                    help="ARC-Top-K, or a comparison compressor of Table I in the same step")
-    ap.add_argument("--batches", type=int, default=4,
-                    help="distinct gradient batches kept resident and cycled")
-    ap.add_argument("--workers", type=int, default=0,
-                    help="override the workload's simulated worker count N (1: one "
-                         "rank's share of a multi-GPU run, the streaming stage at its "
-                         "real shape with nothing to sum over workers)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-model-step", action="store_true",
-                    help="skip the extra timing of the full EF21M iteration with Adam")
-    ap.add_argument("--print-kernel-digest", action="store_true",
-                    help="print the digest of the sketch kernel source and exit")
-    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
-                    help="instead of the compressor, time a plain device copy of GIB "
-                         "gibibytes (empirical bandwidth ceiling; counter calibration)")
-    args = ap.parse_args()
-    if args.print_kernel_digest:
-        print(kernel_source_digest())
-        return
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one MI355X: the compressor path here is single-GPU "
-              "(workers are simulated on the device); run with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+def host_info():
+    """Host cores and memory at the time of the CPU baseline."""
+    info = {"nproc": os.cpu_count()}
+    try:
+        info["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except AttributeError:
+        pass
+    try:
+        with open("/proc/meminfo") as f:
+            mem = {ln.split(":")[0]: int(ln.split()[1]) for ln in f if ln.split()[1].isdigit()}
+        info["mem_total_GB"] = round(mem["MemTotal"] * 1024 / 1e9, 1)
+        info["mem_available_GB"] = round(mem["MemAvailable"] * 1024 / 1e9, 1)
+    except (OSError, KeyError, IndexError, ValueError):
+        pass
+    return info
 
-    if args.steps < 1 or args.warmup < 0:
-        ap.error("--steps must be at least 1 and --warmup at least 0")
 
-    import torch
-
-    if args.copy_calibration > 0:
-        copy_calibration(torch, args.copy_calibration, max(args.steps, 1))
-        return
-
-    import paper_2510_26709_amd as arc
-    import synth
-
-    w = synth.WORKLOADS[args.workload]
-    if args.workers > 0 and args.workers != w.N:
-        import dataclasses
-        w = dataclasses.replace(w, name=f"{w.name}_N{args.workers}", N=args.workers)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    stream = torch.cuda.Stream(dev)
+def measure(torch, arc, synth, w, args, dev, stream, *, with_model, with_cpu):
+    """Time one workload: args.warmup untimed steps, then args.steps timed
+    steps (the value), as many with the library's stage events (stage
+    breakdown, the streaming kernel's mean launch time) and as many with an
+    event after each step (spread).  Returns the workload's report."""
     gen = synth.Generator.for_workload(w)
     gdt = torch.int16 if w.grad_dtype == "bf16" else torch.float32
     nb = max(1, min(args.batches, args.steps + args.warmup))
@@ -351,56 +328,28 @@ def main():
         evs[-1].synchronize()
         per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
         model = None
-        if not args.no_model_step and args.compressor != "topk":
+        if with_model and args.compressor != "topk":
             model = model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb,
                                       args.warmup + 3 * args.steps)
     ms_per_step = total_ms / args.steps
     stages = {name: stage_ms[i] / max(nsteps, 1) for i, name in enumerate(arc.STAGE_NAMES)}
-    log("[bench] ms/step %.4f; stages %s" % (ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
+    log("[bench] %s ms/step %.4f; stages %s" %
+        (w.name, ms_per_step, {k: round(v, 4) for k, v in stages.items()}))
 
-    comp_desc = comp.describe()
     byt = algorithmic_bytes(w, comp.K_total, args.compressor)
-    comm = table1_communication(w, comp, args.compressor)
     sk_ms = stages["sketch"]
     achieved = byt["sketch_kernel"] / (sk_ms * 1e-3) / 1e9
     # The committed counters cover the ARC sketch kernel only.
     traffic = kernel_traffic(w) if args.compressor == "arc" else None
-    value = w.N * w.d / (ms_per_step * 1e-3)
     step_gbps = byt["step"] / (ms_per_step * 1e-3) / 1e9
-
-    # An empirical ceiling beside the vendor peak: a plain 2 GiB device copy
-    # (torch's copy_, the runtime's copy kernel), timed in the same process.
-    nbytes, copy_ms = time_copy(torch, 2, 10)
-    copy_gbps = 2 * nbytes / (copy_ms * 1e-3) / 1e9
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle) ...")
-        cpu = cpu_baseline(w, grads)
-        log(f"[bench] cpu baseline {cpu['value']:.3e} elements/s on {cpu['cores']} threads")
-        if w.name == "tiny":
-            # the smallest workload is also reported on one thread
-            one = cpu_baseline(w, grads, seconds_target=6.0, threads=1)
-            cpu["single_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
-            log(f"[bench] cpu baseline {one['value']:.3e} elements/s on 1 thread")
-    comp.close()
-
-    out = {
-        "metric": "arc_step gradient elements/s and achieved HBM GB/s (% of peak), 1 MI355X",
-        "value": value,
+    rep = {
+        "value": w.N * w.d / (ms_per_step * 1e-3),
         "unit": "gradient elements/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
         "config": {"workload": w.name, "d": w.d, "N": w.N, "n": w.n, "r": w.r, "m": comp.m,
-                   "K_rows": comp.K_total, "grad_dtype": w.grad_dtype, "eta": w.eta,
-                   "mu": w.mu, "buckets": 0 if w.buckets() is None else len(w.buckets()[1]),
+                   "K_rows": comp.K_total, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
+                   "eta": w.eta, "mu": w.mu,
+                   "buckets": 0 if w.buckets() is None else len(w.buckets()[1]),
                    "view": "per_tensor" if w.per_tensor else "single",
                    "compressor": args.compressor,
                    "tensors": len(w.views) if w.per_tensor else 0,
@@ -412,7 +361,7 @@ def main():
         "step_hbm_GBps": step_gbps,
         "step_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "stage_ms": stages,
-        "path": comp_desc,
+        "path": comp.describe(),
         "roofline": {
             "bound": "hbm",
             "kernel": {"arc": "sketch stage: sketch_per_worker_kernel launches (momentum + "
@@ -429,23 +378,143 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": byt["sketch_kernel"],
             "mean_launch_ms": sk_ms,
-            "copy_ceiling": {"GBps": copy_gbps, "bytes_read_plus_written": 2 * nbytes,
-                             "kernel": "device-to-device copy (torch copy_)",
-                             "achieved_over_copy": achieved / copy_gbps},
-        },
-        "cpu_baseline": cpu,
-        "paper_context": {
-            "what": "mean wall-clock time of a whole LLaMA-1B pre-training iteration with Adam "
-                    "(Sec. VI, Table 5): 4x NVIDIA A100 40GB, NCCL over shared memory, "
-                    "NVLink disabled, mu=0.2, r=4; not comparable to this single-GPU "
-                    "compressor step",
-            "s_per_iteration": {"dense": 3.0854, "topk": 2.9628, "randk": 0.9581,
-                                "arc_topk": 1.2130},
-            "arc_vs_dense": -0.6069,
         },
         "ef21m_iteration": model,
-        "communication_per_node": comm,
+        "communication_per_node": table1_communication(w, comp, args.compressor),
     }
+    cpu = None
+    if with_cpu:
+        log(f"[bench] {w.name} cpu baseline (oracle) ...")
+        host = host_info()
+        cpu = cpu_baseline(w, grads)
+        cpu.update(host)
+        log(f"[bench] cpu baseline {cpu['value']:.3e} elements/s on {cpu['cores']} threads")
+        if w.name == "tiny":
+            # the smallest workload is also reported on one thread
+            one = cpu_baseline(w, grads, seconds_target=6.0, threads=1)
+            cpu["single_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
+            log(f"[bench] cpu baseline {one['value']:.3e} elements/s on 1 thread")
+    rep["cpu_baseline"] = cpu
+    comp.close()
+    del grads, h, g
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rep
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--also", default=None,
+                    help="comma-separated further workloads timed in the same run and "
+                         "reported under 'configs' (default: gpt2s beside llama1b, the "
+                         "two configurations the HBM target names; '' for none)")
+    ap.add_argument("--compressor", default="arc", choices=["arc", "randk", "topk"],
+                    help="ARC-Top-K, or a comparison compressor of Table I in the same step")
+    ap.add_argument("--batches", type=int, default=4,
+                    help="distinct gradient batches kept resident and cycled")
+    ap.add_argument("--workers", type=int, default=0,
+                    help="override the workload's simulated worker count N (1: one "
+                         "rank's share of a multi-GPU run, the streaming stage at its "
+                         "real shape with nothing to sum over workers)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-model-step", action="store_true",
+                    help="skip the extra timing of the full EF21M iteration with Adam")
+    ap.add_argument("--print-kernel-digest", action="store_true",
+                    help="print the digest of the sketch kernel source and exit")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="instead of the compressor, time a plain device copy of GIB "
+                         "gibibytes (empirical bandwidth ceiling; counter calibration)")
+    args = ap.parse_args()
+    if args.print_kernel_digest:
+        print(kernel_source_digest())
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X: the compressor path here is single-GPU "
+              "(workers are simulated on the device); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
+
+    import synth
+    if args.workload not in synth.WORKLOADS:
+        ap.error(f"unknown workload {args.workload!r}")
+    if args.also is None:
+        also = ["gpt2s"] if args.workload == "llama1b" and args.compressor == "arc" \
+            and args.workers <= 0 else []
+    else:
+        also = [a for a in args.also.split(",") if a]
+    for a in also:
+        if a not in synth.WORKLOADS:
+            ap.error(f"unknown workload {a!r} in --also")
+
+    import torch
+
+    if args.copy_calibration > 0:
+        copy_calibration(torch, args.copy_calibration, max(args.steps, 1))
+        return
+
+    import paper_2510_26709_amd as arc
+
+    def sized(name):
+        w = synth.WORKLOADS[name]
+        if args.workers > 0 and args.workers != w.N:
+            import dataclasses
+            w = dataclasses.replace(w, name=f"{w.name}_N{args.workers}", N=args.workers)
+        return w
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(dev)
+    w = sized(args.workload)
+    main_rep = measure(torch, arc, synth, w, args, dev, stream,
+                       with_model=not args.no_model_step, with_cpu=not args.no_cpu_baseline)
+    others = {}
+    for name in also:
+        others[name] = measure(torch, arc, synth, sized(name), args, dev, stream,
+                               with_model=False, with_cpu=not args.no_cpu_baseline)
+
+    # An empirical ceiling beside the vendor peak: a plain 2 GiB device copy
+    # (torch's copy_, the runtime's copy kernel), timed in the same process.
+    nbytes, copy_ms = time_copy(torch, 2, 10)
+    copy_gbps = 2 * nbytes / (copy_ms * 1e-3) / 1e9
+    main_rep["roofline"]["copy_ceiling"] = {
+        "GBps": copy_gbps, "bytes_read_plus_written": 2 * nbytes,
+        "kernel": "device-to-device copy (torch copy_)",
+        "achieved_over_copy": main_rep["roofline"]["achieved"] / copy_gbps}
+
+    out = {
+        "metric": "arc_step gradient elements/s and achieved HBM GB/s (% of peak), 1 MI355X",
+        "value": main_rep["value"],
+        "unit": "gradient elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_rep["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        # the arithmetic type of every step; the gradients' storage type is
+        # config.grad_dtype
+        "dtype": "f32",
+        "data": "synthetic",
+    }
+    out.update({k: v for k, v in main_rep.items() if k not in ("value", "unit", "ms_per_step")})
+    out["paper_context"] = {
+        "what": "mean wall-clock time of a whole LLaMA-1B pre-training iteration with Adam "
+                "(Sec. VI, Table 5): 4x NVIDIA A100 40GB, NCCL over shared memory, "
+                "NVLink disabled, mu=0.2, r=4; not comparable to this single-GPU "
+                "compressor step",
+        "s_per_iteration": {"dense": 3.0854, "topk": 2.9628, "randk": 0.9581,
+                            "arc_topk": 1.2130},
+        "arc_vs_dense": -0.6069,
+    }
+    if others:
+        out["configs"] = others
     print(json.dumps(out), flush=True)
 
 

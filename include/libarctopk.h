@@ -173,7 +173,8 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  *   ARC_COMP_TOPK: out_idx is [N][K] (node i's rows at [i*K, (i+1)*K)) and
  *            out_agg [N][L] (node i's rows of Delta^(i), laid out as above),
  *            with K and L one node's row count and payload length.
- * out_idx / out_agg may be NULL only when no row is kept.  With grad, h and
+ * out_idx / out_agg may be NULL only when no row is kept; otherwise they must
+ * not overlap each other or grad, h, g (ARC_ERR_INVALID).  With grad, h and
  * g 16-byte aligned, d % 4 == 0 and r in {1, 2, 4, 8}, rows whose width is a
  * multiple of 4 (per tensor: tensors that also start at a multiple of 4
  * coordinates) take the vectorised path; anything else takes a slower path
@@ -236,7 +237,8 @@ typedef struct {
  *                 h = g = 0)
  *   opt_m, opt_v  device [d] binary32 optimiser state: opt_m for MSGD and
  *                 Adam, opt_v for Adam (start at 0); may be NULL otherwise
- * G, x, opt_m and opt_v must not overlap one another or grad, h, g.
+ * G, x, opt_m and opt_v must not overlap one another, grad, h, g or (on a
+ * compressed iteration) out_idx and out_agg.
  * 16-byte aligned pointers with d % 4 == 0 take the vectorised kernels.
  * Invalid model settings give ARC_ERR_INVALID before any work is enqueued.
  */

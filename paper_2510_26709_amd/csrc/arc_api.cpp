@@ -676,7 +676,7 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
       (st = dev_alloc(&c->gather_dev, c->gather.size(), "hipMalloc(gather)")) ||
       (st = dev_alloc(&c->buckets_dev, nb, "hipMalloc(buckets)")) ||
       (st = dev_alloc(&c->blocks_dev, nblk, "hipMalloc(blocks)")) ||
-      (st = dev_alloc(&c->state_dev, nb, "hipMalloc(state)")) ||
+      (st = dev_alloc(&c->state_dev, arc::kRadixPasses * nb, "hipMalloc(state)")) ||
       (st = dev_alloc(&c->hist_dev, arc::kRadixPasses * nb * arc::kRadixBins,
                       "hipMalloc(hist)")) ||
       (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")) ||
@@ -761,6 +761,21 @@ arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const 
       ranges_overlap(grad, grad_bytes, g, state_bytes) ||
       ranges_overlap(h, state_bytes, g, state_bytes))
     return fail(ARC_ERR_INVALID, "grad, h and g must not overlap");
+  if (need_outputs && c->K_total > 0) {
+    // The gather writes out_agg while it reads h and g of other rows, and
+    // out_idx is read back after the selection wrote it: an alias would
+    // corrupt the state or the payload without an error.
+    const size_t idx_bytes = static_cast<size_t>(c->K_total) * sizeof(int32_t);
+    const size_t agg_bytes = static_cast<size_t>(c->payload) * sizeof(float);
+    if (ranges_overlap(out_idx, idx_bytes, out_agg, agg_bytes))
+      return fail(ARC_ERR_INVALID, "out_idx and out_agg must not overlap");
+    const void* in[3] = {grad, h, g};
+    const size_t in_bytes[3] = {grad_bytes, state_bytes, state_bytes};
+    for (int k = 0; k < 3; ++k)
+      if (ranges_overlap(out_idx, idx_bytes, in[k], in_bytes[k]) ||
+          ranges_overlap(out_agg, agg_bytes, in[k], in_bytes[k]))
+        return fail(ARC_ERR_INVALID, "out_idx and out_agg must not overlap grad, h or g");
+  }
   return ARC_OK;
 }
 
@@ -965,6 +980,10 @@ arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, con
       for (int b = 0; b < 3; ++b)
         if (ranges_overlap(vecs[a], vb, big[b], big_bytes[b]))
           return fail(ARC_ERR_INVALID, "G, x, opt_m, opt_v must not overlap grad, h or g");
+      if (!dense && c->K_total > 0 &&
+          (ranges_overlap(vecs[a], vb, out_idx, static_cast<size_t>(c->K_total) * 4) ||
+           ranges_overlap(vecs[a], vb, out_agg, static_cast<size_t>(c->payload) * 4)))
+        return fail(ARC_ERR_INVALID, "G, x, opt_m, opt_v must not overlap out_idx or out_agg");
     }
   }
 

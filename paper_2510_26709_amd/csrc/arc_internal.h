@@ -84,7 +84,7 @@ struct GatherBucket {
 struct SelectWorkspace {
   const BucketDesc* buckets;
   const BlockDesc* blocks;
-  BucketState* state;
+  BucketState* state;  // [kRadixPasses][nb]: slot q holds the state after digit q
   uint32_t* hist;      // [kRadixPasses][nb][kRadixBins], zero between steps
   uint32_t* blockcnt;  // [nblk][2]: keys above / equal to the threshold
   int32_t nb, nblk;

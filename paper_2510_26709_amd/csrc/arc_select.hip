@@ -7,11 +7,13 @@
 //   pass 0..2  each block histograms, in LDS, the digit of the keys that share
 //              the digits already fixed and adds its non-zero bins to the
 //              bucket's global histogram of that pass (integer atomics);
-//   pass p > 0 first fixes digit p-1: every block of the bucket walks the
-//              previous histogram from the top bin down to the bin holding the
-//              kleft-th largest remaining key (all blocks reach the same
-//              answer; the bucket's first block records it for the next
-//              kernel);
+//   pass p > 0 first fixes digit p-1: every block of the bucket reads the
+//              radix state after digit p-2 (slot p-2, written by the previous
+//              kernel) and walks the previous histogram from the top bin down
+//              to the bin holding the kleft-th largest remaining key (all
+//              blocks reach the same answer); the bucket's first block records
+//              the new state in slot p-1, which no block of the same launch
+//              reads;
 //   count      fixes the last digit (the threshold key T and how many keys
 //              equal to T are kept) and counts, per block, keys above and equal
 //              to T;
@@ -19,8 +21,10 @@
 //              its ties by row, writes the selected rows in order with
 //              block-wide prefix sums, and clears the histograms for the next
 //              step.
-// No kernel waits on another block: there are no grid-wide counters, and the
-// result does not depend on scheduling.
+// No kernel waits on another block: there are no grid-wide counters, every
+// global location a kernel reads was written by an earlier launch on the
+// stream (the state slots are per pass for this reason), and the result does
+// not depend on scheduling.
 //
 // When every bucket has at most kSmallBucketRows rows, one launch of
 // select_small_kernel does all of this instead, one 1024-thread workgroup per
@@ -96,8 +100,15 @@ __device__ BucketState fix_digit(const uint32_t* gh, BucketState st) {
   return st;
 }
 
+// Radix state of bucket b after digits 0..q (slot q of the per-pass states).
+__device__ __forceinline__ BucketState* state_slot(const SelectWorkspace& ws, int q, int32_t b) {
+  return ws.state + (int64_t)q * ws.nb + b;
+}
+
 // Radix state entering pass PASS (digits 0..PASS-1 fixed), computed by wave 0
-// and shared with the block.  The bucket's first block stores it.
+// and shared with the block.  It starts from slot PASS-2, written by the
+// previous kernel, and the bucket's first block stores the result in slot
+// PASS-1 for the next kernel: no slot is both read and written in a launch.
 template <int PASS>
 __device__ BucketState state_before_pass(const SelectWorkspace& ws,
                                          const BucketDesc& bk, int32_t b) {
@@ -109,12 +120,12 @@ __device__ BucketState state_before_pass(const SelectWorkspace& ws,
       st.mask = 0u;
       st.kleft = bk.k;
     } else {
-      st = ws.state[b];
+      st = *state_slot(ws, PASS - 2, b);
     }
     if constexpr (PASS >= 1) st = fix_digit<PASS - 1>(hist_of(ws, PASS - 1, b), st);
     if (threadIdx.x == 0) {
       sh = st;
-      if (PASS >= 1 && (int32_t)blockIdx.x == bk.first_blk) ws.state[b] = st;
+      if (PASS >= 1 && (int32_t)blockIdx.x == bk.first_blk) *state_slot(ws, PASS - 1, b) = st;
     }
   }
   __syncthreads();
@@ -225,7 +236,7 @@ select_write_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
       out_idx[bk.out_off + (p - bk.lo)] = (int32_t)p;
     return;
   }
-  const BucketState st = ws.state[bd.bucket];
+  const BucketState st = *state_slot(ws, kRadixPasses - 1, bd.bucket);
   const uint32_t T = st.prefix;
   const uint64_t kleft = (uint64_t)st.kleft;
   // Keys above / equal to T in the bucket's earlier blocks.

@@ -264,6 +264,15 @@ def test_step_rejects_overlapping_buffers():
             arc.arc_step(comp.ctx, 0, g, h, g, comp.idx, comp.agg)
         with pytest.raises(arc.ArcError, match="t must be"):
             arc.arc_step(comp.ctx, -1, torch.zeros_like(h), h, g, comp.idx, comp.agg)
+        # outputs aliasing each other or the state: rejected before any work
+        grad = torch.ones((N, d), device="cuda")
+        h0, g0 = h.clone(), g.clone()
+        for idx, agg in ((h, comp.agg), (comp.idx, g), (grad, comp.agg), (comp.idx, grad),
+                         (comp.idx, comp.idx), (comp.agg[1:], comp.agg)):
+            with pytest.raises(arc.ArcError, match="overlap"):
+                arc.arc_step(comp.ctx, 0, grad, h, g, idx, agg)
+        torch.cuda.synchronize()
+        assert torch.equal(h, h0) and torch.equal(g, g0)
     finally:
         comp.close()
 
