@@ -61,6 +61,8 @@ def _load():
                                             _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
         "oracle_step_topk_tensors": (ctypes.c_int, [_i32, _f32, _i32, _vp, _vp, _vp, _vp, _i32,
                                                     _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "oracle_merge_topk_rows": (ctypes.c_int, [_i32, _i64, _i64, _i64, _vp, _vp, _vp]),
+        "oracle_merge_topk_tensors": (ctypes.c_int, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
         "oracle_num_threads": (ctypes.c_int, []),
         "oracle_set_num_threads": (None, [ctypes.c_int]),
     }
@@ -304,6 +306,28 @@ def accumulate(G: np.ndarray, idx: np.ndarray, agg: np.ndarray, *, n: int = 0,
         rows, cols, ks = (np.ascontiguousarray(tens[:, c]) for c in range(3))
         _check(_load().oracle_accumulate_tensors(len(rows), _ptr(rows), _ptr(cols), _ptr(ks),
                                                  _ptr(idx), _ptr(agg), _ptr(G)), "accumulate")
+
+
+def merge_topk(G: np.ndarray, idx: np.ndarray, agg: np.ndarray, *, n: int = 0,
+               tensors=None) -> None:
+    """Top-K's merge into G (in place): idx [N, K_node] and agg [N, L] as
+    step_topk returns them; for every coordinate, the values of the nodes that
+    kept its row, summed in ascending node order, are added to G."""
+    _f32c(G, "G")
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    agg = np.ascontiguousarray(agg, dtype=np.float32)
+    if idx.ndim != 2 or agg.ndim != 2 or idx.shape[0] != agg.shape[0]:
+        raise ValueError("idx must be [N, K_node] and agg [N, L]")
+    N = idx.shape[0]
+    if tensors is None:
+        if agg.shape[1] != idx.shape[1] * n:
+            raise ValueError("agg must hold K_node rows of n values per node")
+        _check(_load().oracle_merge_topk_rows(N, G.shape[0], n, idx.shape[1], _ptr(idx),
+                                              _ptr(agg), _ptr(G)), "merge_topk")
+    else:
+        rows, cols, ks = _tensor_arrays(tensors)
+        _check(_load().oracle_merge_topk_tensors(N, len(rows), _ptr(rows), _ptr(cols), _ptr(ks),
+                                                 _ptr(idx), _ptr(agg), _ptr(G)), "merge_topk")
 
 
 def optimizer_step(name: str, G: np.ndarray, x: np.ndarray, m=None, v=None, *, N: int, T: int,

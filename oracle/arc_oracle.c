@@ -544,6 +544,131 @@ int oracle_accumulate_tensors(int32_t num_tensors, const int64_t *rows,
   return 0;
 }
 
+/* Top-K's merge step (Sec. III, "System-Level Limitations of Top-K", and
+ * Prop. 1): after the All-Gather every node holds the N sparse payloads
+ * C_local(Delta^(i)) and sums them, C(g) = (1/N) sum_i C_local(g^(i)); the
+ * nodes keep the sum G = sum_i g^(i).  Written out per coordinate e of row p:
+ * the nodes i that kept row p, in ascending i, contribute their value of e;
+ * the contributions are summed (the first as it is, then plain additions)
+ * and the sum is added to G[e].  Rows no node kept leave G unchanged.  Node
+ * i's list is idx[i*K_node .. +K_node) (rows of the view, as oracle_step_topk
+ * returns them) with payload agg[i*L + q*w ..] for its q-th row of width w.
+ * When every node keeps the same rows this is G += agg of the shared-row
+ * compressors, whose payload is the same ascending sum. */
+static int tensor_buckets(int32_t num_tensors, const int64_t *rows, const int64_t *cols,
+                          const int64_t *K, int64_t *d_out, int64_t *m_out,
+                          int64_t **begin_out);
+
+static int merge_topk(int32_t N, int64_t m, const int64_t *row_off, const int64_t *row_len,
+                      const int64_t *slot_of_pos, int64_t K_node, const int32_t *idx,
+                      const float *agg, int64_t L, float *G) {
+  int64_t *pos = (int64_t *)malloc((size_t)(N * m) * sizeof(int64_t));
+  if (pos == NULL) return 1;
+  for (int64_t k = 0; k < (int64_t)N * m; ++k) pos[k] = -1;
+  for (int32_t i = 0; i < N; ++i)
+    for (int64_t q = 0; q < K_node; ++q) {
+      const int64_t p = idx[(int64_t)i * K_node + q];
+      if (p < 0 || p >= m || pos[(int64_t)i * m + p] >= 0) {
+        free(pos);
+        return 1;
+      }
+      pos[(int64_t)i * m + p] = q;
+    }
+  for (int64_t p = 0; p < m; ++p)
+    for (int64_t j = 0; j < row_len[p]; ++j) {
+      float acc = 0.0f;
+      int have = 0;
+      for (int32_t i = 0; i < N; ++i) {
+        const int64_t q = pos[(int64_t)i * m + p];
+        if (q < 0) continue;
+        const float c = agg[(int64_t)i * L + slot_of_pos[q] + j];
+        acc = have ? acc + c : c;
+        have = 1;
+      }
+      if (have) G[row_off[p] + j] = G[row_off[p] + j] + acc;
+    }
+  free(pos);
+  return 0;
+}
+
+int oracle_merge_topk_rows(int32_t N, int64_t d, int64_t n, int64_t K_node,
+                           const int32_t *idx, const float *agg, float *G) {
+  if (N < 1 || d < 1 || n < 1 || K_node < 0 || G == NULL) return 1;
+  if (K_node > 0 && (idx == NULL || agg == NULL)) return 1;
+  const int64_t m = ceil_div(d, n);
+  if (K_node > m) return 1;
+  int64_t *row_off = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *row_len = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *slot = (int64_t *)malloc((size_t)(K_node > 0 ? K_node : 1) * sizeof(int64_t));
+  int rc = 1;
+  if (row_off && row_len && slot) {
+    for (int64_t p = 0; p < m; ++p) {
+      row_off[p] = p * n;
+      row_len[p] = p * n + n <= d ? n : d - p * n;
+    }
+    for (int64_t q = 0; q < K_node; ++q) slot[q] = q * n;
+    rc = merge_topk(N, m, row_off, row_len, slot, K_node, idx, agg, K_node * n, G);
+  }
+  free(row_off);
+  free(row_len);
+  free(slot);
+  return rc;
+}
+
+int oracle_merge_topk_tensors(int32_t N, int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K, const int32_t *idx,
+                              const float *agg, float *G) {
+  int64_t d, m, *begin = NULL;
+  if (N < 1 || G == NULL) return 1;
+  if (tensor_buckets(num_tensors, rows, cols, K, &d, &m, &begin)) return 1;
+  int64_t K_node = 0, L = 0;
+  for (int32_t b = 0; b < num_tensors; ++b) {
+    const int64_t kb = K[b] < rows[b] ? K[b] : rows[b];
+    K_node += kb;
+    L += kb * cols[b];
+  }
+  int64_t *row_off = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *row_len = (int64_t *)malloc((size_t)m * sizeof(int64_t));
+  int64_t *slot = (int64_t *)malloc((size_t)(K_node > 0 ? K_node : 1) * sizeof(int64_t));
+  int rc = 1;
+  if (row_off && row_len && slot && (K_node == 0 || (idx != NULL && agg != NULL))) {
+    int64_t off = 0, p = 0, q = 0, a0 = 0;
+    for (int32_t b = 0; b < num_tensors; ++b) {
+      for (int64_t r = 0; r < rows[b]; ++r, ++p) {
+        row_off[p] = off + r * cols[b];
+        row_len[p] = cols[b];
+      }
+      off += rows[b] * cols[b];
+      const int64_t kb = K[b] < rows[b] ? K[b] : rows[b];
+      for (int64_t r = 0; r < kb; ++r, ++q, a0 += cols[b]) slot[q] = a0;
+    }
+    /* A node's q-th kept row must lie in the tensor whose list holds q. */
+    int ok = 1;
+    {
+      int64_t q0 = 0, row0 = 0;
+      for (int32_t b = 0; b < num_tensors && ok; ++b) {
+        const int64_t kb = K[b] < rows[b] ? K[b] : rows[b];
+        for (int32_t i = 0; i < N && ok; ++i)
+          for (int64_t r = 0; r < kb; ++r) {
+            const int64_t pr = (int64_t)idx[(int64_t)i * K_node + q0 + r];
+            if (pr < row0 || pr >= row0 + rows[b]) {
+              ok = 0;
+              break;
+            }
+          }
+        q0 += kb;
+        row0 += rows[b];
+      }
+    }
+    if (ok) rc = merge_topk(N, m, row_off, row_len, slot, K_node, idx, agg, L, G);
+  }
+  free(row_off);
+  free(row_len);
+  free(slot);
+  free(begin);
+  return rc;
+}
+
 /* Model update x_{t+1} from G_t, coordinate by coordinate.  The direction is
  * the node average plus the L2 term: dir = fmaf(wd, x, G / N).
  *   SGD  (Eq. (11c)):  x = fmaf(-lr, dir, x)

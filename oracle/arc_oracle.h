@@ -152,6 +152,17 @@ int oracle_step_topk_tensors(int32_t N, float eta, int32_t num_tensors, const in
                              float *agg, int64_t *K_total, int64_t *agg_len,
                              float *norms_out);
 
+/* Top-K's merge into G = sum_i g^(i) (Sec. III, Prop. 1): for every
+ * coordinate of a row some node kept, the kept values of the nodes that kept
+ * it are summed in ascending node order (first value as it is, then plain
+ * additions) and the sum is added to G.  idx and agg as oracle_step_topk (and
+ * _tensors) return them: [N][K_node] rows of the view, [N][L] payload. */
+int oracle_merge_topk_rows(int32_t N, int64_t d, int64_t n, int64_t K_node,
+                           const int32_t *idx, const float *agg, float *G);
+int oracle_merge_topk_tensors(int32_t N, int32_t num_tensors, const int64_t *rows,
+                              const int64_t *cols, const int64_t *K, const int32_t *idx,
+                              const float *agg, float *G);
+
 /* Number of threads the oracle's parallel loops use. */
 int oracle_num_threads(void);
 void oracle_set_num_threads(int n);

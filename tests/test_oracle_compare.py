@@ -198,3 +198,134 @@ def test_topk_single_node_is_the_exact_row_top_k():
     out = oracle.step_topk(np.zeros_like(x), np.zeros_like(x), x, eta=1.0, n=n, K=K)
     norms = (x.astype(np.float64).reshape(m, n) ** 2).sum(axis=1)
     assert np.array_equal(out["idx"][0], np.sort(np.argsort(-norms)[:K]))
+
+
+# ---------------------------------------------------- Top-K merge into G --
+
+def test_topk_merge_prop1_worked_example():
+    # Prop. 1: the merged local selections cancel; G (the node sum) stays
+    # [0, 0] while the sum of the gradients is [0, 0.2]: C(g) = 0, so the
+    # error is ||g||^2.
+    gd = _golden("prop1_example.txt")
+    grad = np.array([[float(v) for v in gd["grad0"][0]], [float(v) for v in gd["grad1"][0]]], F32)
+    h, g = np.zeros((2, 2), F32), np.zeros((2, 2), F32)
+    out = oracle.step_topk(h, g, grad, eta=1.0, n=1, K=1)
+    G = np.zeros(2, F32)
+    oracle.merge_topk(G, out["idx"], out["agg"], n=1)
+    mean = G.astype(np.float64) / 2
+    assert np.array_equal(mean, np.array([float(v) for v in gd["local_topk_mean"][0]]))
+    g_mean = grad.astype(np.float64).mean(axis=0)
+    assert np.sum((mean - g_mean) ** 2) == pytest.approx(np.sum(g_mean ** 2))
+
+
+def test_topk_merge_small_integers_brute_force():
+    # Small integers are exact in binary32, so the merge must equal the exact
+    # scatter-add of every node's kept rows (overlapping and disjoint rows,
+    # a ragged last row).
+    rng = np.random.default_rng(12)
+    for N, n, m, K in ((3, 5, 40, 9), (5, 8, 12, 12), (2, 1, 30, 30), (4, 7, 20, 1)):
+        d = n * m - (n // 2)
+        idx = np.stack([np.sort(rng.choice(m, K, replace=False)) for _ in range(N)]).astype(
+            np.int32)
+        agg = rng.integers(-50, 50, size=(N, K * n)).astype(F32)
+        for i in range(N):  # payload past d is +0 (as step_topk writes it)
+            for q in range(K):
+                p = idx[i, q]
+                for j in range(n):
+                    if p * n + j >= d:
+                        agg[i, q * n + j] = 0.0
+        G0 = rng.integers(-1000, 1000, size=d).astype(F32)
+        G = G0.copy()
+        oracle.merge_topk(G, idx, agg, n=n)
+        want = G0.astype(np.int64)
+        for i in range(N):
+            for q in range(K):
+                p = idx[i, q]
+                for j in range(n):
+                    if p * n + j < d:
+                        want[p * n + j] += int(agg[i, q * n + j])
+        assert np.array_equal(G.astype(np.int64), want), (N, n, m, K)
+
+
+def test_topk_merge_sums_nodes_in_ascending_order_before_adding():
+    # All three nodes keep row 0 with values 2^24, 1, -2^24: ascending sum
+    # (2^24 + 1) - 2^24 rounds to 0 (descending would give 1).  Then with
+    # G = 2^24 and two nodes adding 1 each: the sum first gives 2^24 + 2,
+    # adding one at a time into G would leave 2^24.
+    idx = np.zeros((3, 1), np.int32)
+    agg = np.array([[2.0 ** 24], [1.0], [-(2.0 ** 24)]], F32)
+    G = np.zeros(1, F32)
+    oracle.merge_topk(G, idx, agg, n=1)
+    assert G[0] == 0.0
+    G = np.array([2.0 ** 24], F32)
+    oracle.merge_topk(G, np.zeros((2, 1), np.int32), np.ones((2, 1), F32), n=1)
+    assert G[0] == 2.0 ** 24 + 2
+
+
+def test_topk_merge_with_shared_rows_is_the_shared_row_accumulate():
+    # Every node keeping the same rows: the merge equals G += (ascending sum
+    # of the payloads) at those rows, the shared-row route.
+    rng = np.random.default_rng(13)
+    N, n, m, K = 4, 6, 25, 8
+    d = n * m
+    rows = np.sort(rng.choice(m, K, replace=False)).astype(np.int32)
+    idx = np.tile(rows, (N, 1))
+    agg = rng.standard_normal((N, K * n)).astype(F32)
+    G0 = rng.standard_normal(d).astype(F32)
+    G = G0.copy()
+    oracle.merge_topk(G, idx, agg, n=n)
+    summed = agg[0].copy()
+    for i in range(1, N):
+        summed = (summed + agg[i]).astype(F32)
+    G_shared = G0.copy()
+    oracle.accumulate(G_shared, rows, summed, n=n)
+    assert np.array_equal(G.view(np.uint32), G_shared.view(np.uint32))
+
+
+def test_topk_merge_keeping_every_row_is_the_dense_step():
+    # K = m: every node keeps every row, so the merged G is the dense step's
+    # G (the identity compressor), bit for bit.
+    rng = np.random.default_rng(14)
+    N, n, m = 3, 8, 20
+    d = n * m - 3
+    h = rng.standard_normal((N, d)).astype(F32)
+    g = rng.standard_normal((N, d)).astype(F32)
+    grad = rng.standard_normal((N, d)).astype(F32)
+    G0 = rng.standard_normal(d).astype(F32)
+    h1, g1, G1 = h.copy(), g.copy(), G0.copy()
+    out = oracle.step_topk(h1, g1, grad, eta=0.25, n=n, K=m)
+    oracle.merge_topk(G1, out["idx"], out["agg"], n=n)
+    h2, g2, G2 = h.copy(), g.copy(), G0.copy()
+    oracle.dense_step(h2, g2, G2, grad, 0.25)
+    for a, b in ((h1, h2), (g1, g2), (G1, G2)):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_topk_merge_tensors_equal_single_view_when_widths_agree():
+    rng = np.random.default_rng(15)
+    N, w = 3, 16
+    tensors = [(10, w, 3), (7, w, 7), (12, w, 2)]
+    m = sum(r for r, _, _ in tensors)
+    d = m * w
+    h = rng.standard_normal((N, d)).astype(F32)
+    g = rng.standard_normal((N, d)).astype(F32)
+    grad = rng.standard_normal((N, d)).astype(F32)
+    G0 = rng.standard_normal(d).astype(F32)
+    ht, gt, Gt = h.copy(), g.copy(), G0.copy()
+    out_t = oracle.step_topk(ht, gt, grad, eta=0.5, tensors=tensors)
+    oracle.merge_topk(Gt, out_t["idx"], out_t["agg"], tensors=tensors)
+    begin = np.cumsum([0] + [r for r, _, _ in tensors]).tolist()
+    hb, gb, Gb = h.copy(), g.copy(), G0.copy()
+    out_b = oracle.step_topk(hb, gb, grad, eta=0.5, n=w,
+                             buckets=(begin, [k for _, _, k in tensors]))
+    oracle.merge_topk(Gb, out_b["idx"], out_b["agg"], n=w)
+    assert np.array_equal(out_t["idx"], out_b["idx"])
+    assert np.array_equal(Gt.view(np.uint32), Gb.view(np.uint32))
+
+
+def test_topk_merge_rejects_rows_out_of_range_or_repeated():
+    G = np.zeros(20, F32)
+    with pytest.raises(oracle.OracleError):
+        oracle.merge_topk(G, np.array([[0, 5]], np.int32), np.zeros((1, 8), F32), n=4)
+    with pytest.raises(oracle.OracleError):
+        oracle.merge_topk(G, np.array([[1, 1]], np.int32), np.zeros((1, 8), F32), n=4)
