@@ -328,7 +328,7 @@ def measure(torch, arc, synth, w, args, dev, stream, *, with_model, with_cpu):
         evs[-1].synchronize()
         per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
         model = None
-        if with_model and args.compressor != "topk":
+        if with_model:
             model = model_step_timing(torch, arc, w, comp, grads, h, g, stream, nb,
                                       args.warmup + 3 * args.steps)
     ms_per_step = total_ms / args.steps

@@ -224,14 +224,18 @@ typedef struct {
 } arc_model_config;
 
 /*
- * One EF21M iteration (11a)-(11c) on the context's stream (ARC_COMP_ARC and
- * ARC_COMP_RANDK; ARC_COMP_TOPK gives ARC_ERR_UNSUPPORTED).
+ * One EF21M iteration (11a)-(11c) on the context's stream, for every
+ * compressor.
  *   t < dense_steps: the identity compressor (no compression yet): for every
  *     coordinate, Eq. (11a), Delta_i = h_i - g_i, g_i = g_i + Delta_i, and
  *     G = G + (Delta_0 + Delta_1 + ...); out_idx and out_agg are not written.
  *     The same bits as arc_step with every row kept followed by G += agg.
  *   otherwise: arc_step (same outputs), and G = G + agg at the selected
- *     coordinates.
+ *     coordinates.  ARC_COMP_TOPK (Sec. III: the All-Gather is followed by a
+ *     merge): every coordinate of a row that some node kept gets the values
+ *     of the nodes that kept it, summed in ascending node order (the first as
+ *     it is, then plain additions), added to G; with every node keeping the
+ *     same rows, the same bits as the shared-row compressors.
  * Then the optimiser updates x (and opt_m, opt_v) over all d coordinates.
  *   G, x          device [d] binary32, in/out; G starts at sum_i g^(i) (0 for
  *                 h = g = 0)

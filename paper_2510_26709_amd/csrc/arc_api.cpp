@@ -22,12 +22,13 @@
 #include <string>
 #include <vector>
 
-#include "arc_internal.h"
-#include "libarctopk.h"
+#include "arc_context.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace arc {
 
 arc_status fail(arc_status s, const std::string& why) {
   g_last_error = why;
@@ -39,13 +40,13 @@ arc_status fail_hip(hipError_t e, const char* where) {
   return e == hipErrorOutOfMemory ? ARC_ERR_NOMEM : ARC_ERR_DEVICE;
 }
 
-#define ARC_HIP(call, where)                                  \
-  do {                                                        \
-    const hipError_t arc_e_ = (call);                         \
-    if (arc_e_ != hipSuccess) return fail_hip(arc_e_, where); \
-  } while (0)
+}  // namespace arc
 
-constexpr int kEventsPerStep = 6;
+namespace {
+
+using arc::fail;
+using arc::fail_hip;
+
 constexpr int64_t kGroupRows = 64;  // rows of one row group (one wave's rows)
 constexpr int32_t kMaxTensors = 1 << 24;
 
@@ -91,114 +92,6 @@ int32_t vector_group_rows(int64_t cols) {
 
 }  // namespace
 
-struct arc_ctx {
-  // problem
-  int64_t d = 0, n = 0, m = 0;
-  int32_t N = 0, r = 0, grad_bf16 = 0;
-  float eta = 0.f, a = 0.f;
-  uint64_t seed = 0;
-  bool tensor_mode = false;
-  int32_t compressor = ARC_COMP_ARC;
-  // Rows kept and payload floats per step, over all nodes (Top-K returns
-  // every node's rows; the others one shared list), and for one node.
-  int64_t K_total = 0, payload = 0, K_node = 0, payload_node = 0;
-  std::vector<arc::BucketDesc> buckets;
-  std::vector<arc::BlockDesc> blocks;
-  // projection: one V_t per distinct row width, concatenated in first-use order
-  std::vector<int64_t> widths;
-  std::map<int64_t, int64_t> v_off;
-  int64_t v_floats = 0;
-  // row groups: the vectorisable ones by group size (64, 32, 16 rows), then
-  // the general ones
-  std::vector<arc::RowGroup> groups;
-  int64_t nvec_groups = 0;
-  std::array<int64_t, 4> vec_count{};  // groups of 64, 32, 16 and 8 rows
-  std::array<int64_t, 5> stage_elems{};  // coordinates per launch: those sizes, general
-  std::array<arc::SketchOccupancy, 4> vec_occ{};  // launch shape per group size
-  // per-tensor gather
-  std::vector<arc::GatherBucket> gather;
-  int64_t gather_work = 0;
-  // device
-  hipStream_t stream = nullptr;
-  // second stream for the smaller launches of the streaming stage, forked
-  // from and joined back into `stream` (only when there are several)
-  hipStream_t side = nullptr;
-  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
-  int device = 0;
-  size_t max_lds_per_block = 0;
-  float* V_dev = nullptr;
-  float* S_dev = nullptr;
-  float* sigma_dev = nullptr;
-  arc::RowGroup* groups_dev = nullptr;
-  int32_t* sel_dev = nullptr;  // Top-K: selection over the N*m norms
-  arc::GatherBucket* gather_dev = nullptr;
-  arc::BucketDesc* buckets_dev = nullptr;
-  arc::BlockDesc* blocks_dev = nullptr;
-  arc::BucketState* state_dev = nullptr;
-  uint32_t* hist_dev = nullptr;
-  uint32_t* blockcnt_dev = nullptr;
-  // projection staging: two pinned buffers, reused every other step; the
-  // pool fills the next step's buffer while the device runs this step
-  float* V_pinned[2] = {nullptr, nullptr};
-  hipEvent_t V_done[2] = {nullptr, nullptr};
-  bool V_pending[2] = {false, false};
-  int V_slot = 0;
-  std::vector<float> V_override;
-  bool use_override = false;
-  std::vector<arc::ProjectionBlock> V_blocks;
-  std::unique_ptr<arc::ProjectionPool> V_pool;
-  int64_t V_prefetch_t = -1;  // step whose V_t the pool put in V_pinned[V_slot]
-  // stage timing
-  bool timing = false;
-  std::vector<std::array<hipEvent_t, kEventsPerStep>> ev_pool;
-  size_t ev_used = 0;
-
-  arc::SelectWorkspace select_ws() const {
-    arc::SelectWorkspace ws;
-    ws.buckets = buckets_dev;
-    ws.blocks = blocks_dev;
-    ws.state = state_dev;
-    ws.hist = hist_dev;
-    ws.blockcnt = blockcnt_dev;
-    ws.nb = static_cast<int32_t>(buckets.size());
-    ws.nblk = static_cast<int32_t>(blocks.size());
-    ws.any_radix = 0;
-    ws.any_output = 0;
-    ws.small = 1;
-    for (const auto& b : buckets) {
-      ws.any_radix |= b.mode == arc::kSelectRadix;
-      ws.any_output |= b.mode != arc::kSelectNone;
-      ws.small &= b.hi - b.lo <= arc::kSmallBucketRows;
-    }
-    return ws;
-  }
-
-  void release() {
-    V_pool.reset();  // joins the threads before their buffers go
-    (void)hipStreamSynchronize(stream);
-    if (side) {
-      (void)hipStreamSynchronize(side);
-      (void)hipStreamDestroy(side);
-    }
-    for (hipEvent_t e : {fork_ev, join_ev})
-      if (e) (void)hipEventDestroy(e);
-    for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
-                    static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
-                    static_cast<void*>(sel_dev),
-                    static_cast<void*>(gather_dev), static_cast<void*>(buckets_dev),
-                    static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
-                    static_cast<void*>(hist_dev), static_cast<void*>(blockcnt_dev)})
-      if (p) (void)hipFree(p);
-    for (int s = 0; s < 2; ++s) {
-      if (V_done[s]) (void)hipEventDestroy(V_done[s]);
-      if (V_pinned[s]) (void)hipHostFree(V_pinned[s]);
-    }
-    for (auto& evs : ev_pool)
-      for (hipEvent_t e : evs)
-        if (e) (void)hipEventDestroy(e);
-    ev_pool.clear();
-  }
-};
 
 namespace {
 
@@ -226,7 +119,7 @@ arc_status check_tensors(const arc_config* cfg, int64_t* m_out) {
 }
 
 // Configuration checks shared by arc_create; no HIP call is made here.
-arc_status check_config(const arc_config* cfg, int64_t* m_out) {
+arc_status check_config_impl(const arc_config* cfg, int64_t* m_out) {
   if (cfg == nullptr) return fail(ARC_ERR_INVALID, "cfg is NULL");
   if (cfg->d <= 0) return fail(ARC_ERR_INVALID, "d must be > 0");
   if (cfg->N <= 0 || cfg->N > 65535) return fail(ARC_ERR_INVALID, "N must be in 1..65535");
@@ -622,30 +515,15 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   if (out == nullptr) return fail(ARC_ERR_INVALID, "out is NULL");
   *out = nullptr;
   int64_t m = 0;
-  arc_status st = check_config(cfg, &m);
+  arc_status st = arc::check_config(cfg, &m);
   if (st != ARC_OK) return st;
-  if (cfg->compressor == ARC_COMP_TOPK && m > INT32_MAX / cfg->N)
-    return fail(ARC_ERR_INVALID, "Top-K: N * m must be below 2^31");
 
   arc_ctx* c = new (std::nothrow) arc_ctx();
   if (c == nullptr) return fail(ARC_ERR_NOMEM, "host allocation failed");
-  try {
-    c->d = cfg->d;
-    c->tensor_mode = cfg->num_tensors > 0;
-    c->compressor = cfg->compressor;
-    c->n = c->tensor_mode ? 0 : cfg->n;
-    c->m = m;
-    c->N = cfg->N;
-    c->r = cfg->r;
-    c->grad_bf16 = cfg->grad_dtype == ARC_DTYPE_BF16;
-    c->eta = cfg->eta;
-    c->a = 1.0f - cfg->eta;
-    c->seed = cfg->seed;
-    c->stream = static_cast<hipStream_t>(hip_stream);
-    build_plan(cfg, c);
-  } catch (...) {
+  st = arc::plan_context(cfg, m, hip_stream, c);
+  if (st != ARC_OK) {
     delete c;
-    return fail(ARC_ERR_NOMEM, "host allocation failed");
+    return st;
   }
 
   auto bail = [&](arc_status s) {
@@ -653,20 +531,8 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
     delete c;
     return s;
   };
-  hipError_t e = hipGetDevice(&c->device);
-  if (e != hipSuccess) return bail(fail_hip(e, "hipGetDevice"));
-  int lds_limit = 0;
-  e = hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device);
-  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
-  c->max_lds_per_block = static_cast<size_t>(lds_limit);
-  // One workgroup per compute unit is reached through the LDS reservation,
-  // which assumes the gfx950 figure; on any other, launches go uncapped.
-  int lds_cu = 0;
-  e = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
-                            c->device);
-  if (e != hipSuccess) return bail(fail_hip(e, "hipDeviceGetAttribute"));
-  if (lds_cu != arc::kLdsPerCu || lds_limit < arc::kLdsPerCu / 2 + 1024)
-    for (auto& o : c->vec_occ) o.one_per_cu = 0;
+  if ((st = arc::bind_device(c)) != ARC_OK) return bail(st);
+  hipError_t e;
 
   const size_t nb = c->buckets.size(), nblk = c->blocks.size();
   if ((st = dev_alloc(&c->V_dev, static_cast<size_t>(c->v_floats), "hipMalloc(V)")) ||
@@ -681,7 +547,10 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
                       "hipMalloc(hist)")) ||
       (st = dev_alloc(&c->blockcnt_dev, 2 * nblk, "hipMalloc(blockcnt)")) ||
       (st = dev_alloc(&c->sel_dev, c->compressor == ARC_COMP_TOPK ? c->K_total : 0,
-                      "hipMalloc(selection)")))
+                      "hipMalloc(selection)")) ||
+      (st = dev_alloc(&c->mark_dev,
+                      c->compressor == ARC_COMP_TOPK ? static_cast<size_t>(c->N) * c->m : 0,
+                      "hipMalloc(merge tags)")))
     return bail(st);
   for (int s = 0; s < 2; ++s) {
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
@@ -722,6 +591,8 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
   if (e == hipSuccess) e = upload(c->gather_dev, c->gather);
   if (e == hipSuccess)
     e = hipMemset(c->hist_dev, 0, arc::kRadixPasses * nb * arc::kRadixBins * sizeof(uint32_t));
+  if (e == hipSuccess && c->compressor == ARC_COMP_TOPK)
+    e = hipMemset(c->mark_dev, 0, static_cast<size_t>(c->N) * c->m * sizeof(uint64_t));
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) return bail(fail_hip(e, "workspace initialisation"));
   *out = c;
@@ -746,7 +617,7 @@ int64_t arc_payload_elems(const arc_ctx* ctx) { return ctx ? ctx->payload : -1; 
 namespace {
 
 // need_outputs: the call writes out_idx / out_agg (every compressed step).
-arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const float* h,
+arc_status check_step_args_impl(const arc_ctx* c, int64_t t, const void* grad, const float* h,
                            const float* g, const int32_t* out_idx, const float* out_agg,
                            bool need_outputs) {
   if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
@@ -842,8 +713,8 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
 
 // The compressor step (arguments already checked); with a non-null G the
 // payload is also added into G at the selected coordinates.
-arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
-                        int32_t* out_idx, float* out_agg, float* G) {
+arc_status enqueue_step_impl(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                             int32_t* out_idx, float* out_agg, float* G) {
   // Vectorisable groups take the 16-byte kernels only when the three streams
   // are 16-byte aligned; otherwise every group takes the general kernel.
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
@@ -852,7 +723,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   size_t slot = 0;
   if (c->timing) {
     if (c->ev_used == c->ev_pool.size()) {
-      std::array<hipEvent_t, kEventsPerStep> evs{};
+      std::array<hipEvent_t, arc::kEventsPerStep> evs{};
       for (auto& e : evs) ARC_HIP(hipEventCreate(&e), "hipEventCreate");
       c->ev_pool.push_back(evs);
     }
@@ -860,7 +731,8 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
   }
   arc_status st;
   if ((st = record(c, slot, 0))) return st;
-  if (c->compressor == ARC_COMP_ARC && (st = upload_projection(c, t))) return st;
+  if (c->compressor == ARC_COMP_ARC && !c->V_staged && (st = upload_projection(c, t)))
+    return st;
   if ((st = record(c, slot, 1))) return st;
   const arc::SelectWorkspace ws = c->select_ws();
   if (c->compressor == ARC_COMP_RANDK) {
@@ -883,14 +755,28 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
     // Stage 2: every node's own top-K over its norms.
     ARC_HIP(arc::launch_select(c->S_dev, ws, c->sel_dev, c->stream), "select launch");
     if ((st = record(c, slot, 4))) return st;
-    // Stage 3: every node's rows, unsummed (the All-Gather payload).
+    // Stage 3: every node's rows, unsummed (the All-Gather payload); in the
+    // model step, tagged per node for the merge that follows.
     const bool vec = c->d % 4 == 0 && c->payload_node % 4 == 0 && aligned16(h) &&
                      aligned16(g) && aligned16(out_agg);
+    const bool merge = G != nullptr && c->mark_dev != nullptr;
+    if (merge && ++c->mark_stamp == 0) {
+      // After 2^32 merges the stamps wrap: clear the old tags first.
+      ARC_HIP(arc::launch_zero_u64(c->mark_dev, static_cast<int64_t>(c->N) * c->m, c->stream),
+              "tag clear launch");
+      c->mark_stamp = 1;
+    }
     ARC_HIP(arc::launch_topk_gather(h, g, c->sel_dev, out_idx, out_agg, c->gather_dev,
                                     static_cast<int32_t>(c->gather.size()), c->gather_work,
                                     c->K_node, c->payload_node, c->d, c->m, c->N, vec,
-                                    c->stream),
+                                    merge ? c->mark_dev : nullptr, c->mark_stamp, c->stream),
             "gather launch");
+    if (merge)
+      ARC_HIP(arc::launch_topk_merge(out_agg, c->sel_dev, c->mark_dev, c->mark_stamp,
+                                     c->gather_dev, static_cast<int32_t>(c->gather.size()),
+                                     c->gather_work, c->K_node, c->payload_node, c->d, c->m,
+                                     c->N, G, c->stream),
+              "merge launch");
     return record(c, slot, 5);
   } else {
     // Stage 0: momentum + residual + per-worker sketch in one HBM stream.
@@ -936,20 +822,18 @@ extern "C" {
 
 arc_status arc_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
                     int32_t* out_idx, float* out_agg) {
-  const arc_status st = check_step_args(c, t, grad, h, g, out_idx, out_agg, true);
+  const arc_status st = arc::check_step_args(c, t, grad, h, g, out_idx, out_agg, true);
   if (st != ARC_OK) return st;
-  return enqueue_step(c, t, grad, h, g, out_idx, out_agg, nullptr);
+  return arc::enqueue_step(c, t, grad, h, g, out_idx, out_agg, nullptr);
 }
 
 arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, const void* grad,
                           float* h, float* g, float* G, float* x, float* opt_m, float* opt_v,
                           int32_t* out_idx, float* out_agg) {
   if (mc == nullptr) return fail(ARC_ERR_INVALID, "model config is NULL");
-  if (c != nullptr && c->compressor == ARC_COMP_TOPK)
-    return fail(ARC_ERR_UNSUPPORTED, "arc_model_step: Top-K payloads are not merged into G");
   // A dense iteration writes no payload, so out_idx / out_agg may be NULL.
   const bool dense = t < mc->dense_steps;
-  arc_status st = check_step_args(c, t, grad, h, g, out_idx, out_agg, !dense);
+  arc_status st = arc::check_step_args(c, t, grad, h, g, out_idx, out_agg, !dense);
   if (st != ARC_OK) return st;
   if (mc->optimizer < ARC_OPT_SGD || mc->optimizer > ARC_OPT_ADAM)
     return fail(ARC_ERR_INVALID, "optimizer must be ARC_OPT_SGD, ARC_OPT_MSGD or ARC_OPT_ADAM");
@@ -994,7 +878,7 @@ arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, con
                                    c->stream),
             "dense step launch");
   } else {
-    st = enqueue_step(c, t, grad, h, g, out_idx, out_agg, G);
+    st = arc::enqueue_step(c, t, grad, h, g, out_idx, out_agg, G);
     if (st != ARC_OK) return st;
   }
 
@@ -1019,7 +903,8 @@ arc_status arc_model_step(arc_ctx* c, const arc_model_config* mc, int64_t t, con
   o.fN = static_cast<float>(c->N);
   const bool vec = c->d % 4 == 0 && aligned16(G) && aligned16(x) &&
                    (o.kind < 1 || aligned16(opt_m)) && (o.kind < 2 || aligned16(opt_v));
-  ARC_HIP(arc::launch_optimizer(vec, o, G, x, opt_m, opt_v, c->d, c->stream),
+  ARC_HIP(arc::launch_optimizer(vec, c->lds_per_cu == arc::kLdsPerCu, o, G, x, opt_m, opt_v,
+                                c->d, c->stream),
           "optimizer launch");
   return ARC_OK;
 }
@@ -1117,7 +1002,7 @@ arc_status arc_timing_read(arc_ctx* c, double* ms, int64_t* steps) {
   for (int k = 0; k < ARC_NUM_STAGES; ++k) ms[k] = 0.0;
   for (size_t s = 0; s < c->ev_used; ++s) {
     auto& ev = c->ev_pool[s];
-    ARC_HIP(hipEventSynchronize(ev[kEventsPerStep - 1]), "hipEventSynchronize");
+    ARC_HIP(hipEventSynchronize(ev[arc::kEventsPerStep - 1]), "hipEventSynchronize");
     float x = 0.f;
     const int pairs[ARC_NUM_STAGES][2] = {{1, 2}, {2, 3}, {3, 4}, {4, 5}, {0, 5}};
     for (int k = 0; k < ARC_NUM_STAGES; ++k) {
@@ -1132,3 +1017,65 @@ arc_status arc_timing_read(arc_ctx* c, double* ms, int64_t* steps) {
 }
 
 }  // extern "C"
+
+namespace arc {
+
+arc_status check_config(const arc_config* cfg, int64_t* m_out) {
+  const arc_status st = check_config_impl(cfg, m_out);
+  if (st != ARC_OK) return st;
+  if (cfg->compressor == ARC_COMP_TOPK && *m_out > INT32_MAX / cfg->N)
+    return fail(ARC_ERR_INVALID, "Top-K: N * m must be below 2^31");
+  return ARC_OK;
+}
+
+arc_status plan_context(const arc_config* cfg, int64_t m, void* stream, arc_ctx* c) {
+  try {
+    c->d = cfg->d;
+    c->tensor_mode = cfg->num_tensors > 0;
+    c->compressor = cfg->compressor;
+    c->n = c->tensor_mode ? 0 : cfg->n;
+    c->m = m;
+    c->N = cfg->N;
+    c->r = cfg->r;
+    c->grad_bf16 = cfg->grad_dtype == ARC_DTYPE_BF16;
+    c->eta = cfg->eta;
+    c->a = 1.0f - cfg->eta;
+    c->seed = cfg->seed;
+    c->stream = static_cast<hipStream_t>(stream);
+    build_plan(cfg, c);
+  } catch (...) {
+    return fail(ARC_ERR_NOMEM, "host allocation failed");
+  }
+  return ARC_OK;
+}
+
+arc_status bind_device(arc_ctx* c) {
+  ARC_HIP(hipGetDevice(&c->device), "hipGetDevice");
+  int lds_limit = 0;
+  ARC_HIP(hipDeviceGetAttribute(&lds_limit, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device),
+          "hipDeviceGetAttribute");
+  c->max_lds_per_block = static_cast<size_t>(lds_limit);
+  // One workgroup per compute unit is reached through the LDS reservation,
+  // which assumes the gfx950 figure; on any other, launches go uncapped.
+  int lds_cu = 0;
+  ARC_HIP(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                c->device),
+          "hipDeviceGetAttribute");
+  c->lds_per_cu = lds_cu;
+  if (lds_cu != kLdsPerCu || lds_limit < kLdsPerCu / 2 + 1024)
+    for (auto& o : c->vec_occ) o.one_per_cu = 0;
+  return ARC_OK;
+}
+
+arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const float* h,
+                           const float* g, const int32_t* out_idx, const float* out_agg,
+                           bool need_outputs) {
+  return check_step_args_impl(c, t, grad, h, g, out_idx, out_agg, need_outputs);
+}
+
+arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                        int32_t* out_idx, float* out_agg, float* G) {
+  return enqueue_step_impl(c, t, grad, h, g, out_idx, out_agg, G);
+}
+
+}  // namespace arc

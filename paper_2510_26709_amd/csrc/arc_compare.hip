@@ -65,34 +65,56 @@ randk_keys_kernel(uint64_t seed, int64_t t, int64_t m, float* __restrict__ keys)
   keys[p] = (float)(uint32_t)(x >> 40);  // an integer below 2^24: exact
 }
 
-// One work item = one selected row x 4 columns of one node (see the
-// launcher).  Each node's rows are its own; nothing is summed.
-__global__ void __launch_bounds__(256)
-topk_gather_kernel(const float* __restrict__ h, float* __restrict__ g,
-                   const int32_t* __restrict__ sel, int32_t* __restrict__ out_idx,
-                   float* __restrict__ agg, const GatherBucket* __restrict__ buckets,
-                   int32_t nb, int64_t work, int64_t K_total, int64_t payload, int64_t d,
-                   int64_t m, int32_t N, int32_t vec) {
-  const int64_t w_all = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (w_all >= (int64_t)N * work) return;
-  const int64_t i = w_all / work, w = w_all - i * work;
+// Work item w of node i (one selected row x 4 columns): its bucket, the
+// row's position q within the bucket's list, and the first column.
+struct TopkItem {
+  GatherBucket bk;
+  int64_t q, col;
+};
+
+__device__ __forceinline__ TopkItem topk_item(const GatherBucket* __restrict__ buckets,
+                                              int32_t nb, int64_t w) {
   int32_t lo = 0, hi = nb;  // last bucket whose work_off <= w
   while (hi - lo > 1) {
     const int32_t mid = (lo + hi) >> 1;
     if (buckets[mid].work_off <= w) lo = mid; else hi = mid;
   }
-  const GatherBucket bk = buckets[lo];
-  const int64_t per_row = (bk.cols + 3) / 4;
-  const int64_t item = w - bk.work_off;
-  const int64_t q = item / per_row;
-  const int64_t col = (item - q * per_row) * 4;
+  TopkItem it;
+  it.bk = buckets[lo];
+  const int64_t per_row = (it.bk.cols + 3) / 4;
+  const int64_t item = w - it.bk.work_off;
+  it.q = item / per_row;
+  it.col = (item - it.q * per_row) * 4;
+  return it;
+}
+
+// One work item = one selected row x 4 columns of one node (see the
+// launcher).  Each node's rows are its own; nothing is summed.  With `mark`
+// (the model step), node i's row p is tagged mark[i*m + p] = stamp << 32 | q
+// for the merge that follows.
+__global__ void __launch_bounds__(256)
+topk_gather_kernel(const float* __restrict__ h, float* __restrict__ g,
+                   const int32_t* __restrict__ sel, int32_t* __restrict__ out_idx,
+                   float* __restrict__ agg, const GatherBucket* __restrict__ buckets,
+                   int32_t nb, int64_t work, int64_t K_total, int64_t payload, int64_t d,
+                   int64_t m, int32_t N, int32_t vec, uint64_t* __restrict__ mark,
+                   uint32_t stamp) {
+  const int64_t w_all = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (w_all >= (int64_t)N * work) return;
+  const int64_t i = w_all / work, w = w_all - i * work;
+  const TopkItem it = topk_item(buckets, nb, w);
+  const GatherBucket& bk = it.bk;
+  const int64_t q = it.q, col = it.col;
   const int64_t pos = i * K_total + bk.out_off + q;
   const int64_t p = (int64_t)sel[pos] - i * m;  // row of the view
   const int64_t pr = p - bk.row0;               // row within the bucket
   // Only this node's rows of this bucket; the bounds keep a broken index from
   // touching memory outside the vectors.
   if (q >= bk.k || pr < 0 || pr >= bk.rows) return;
-  if (col == 0) out_idx[pos] = (int32_t)p;
+  if (col == 0) {
+    out_idx[pos] = (int32_t)p;
+    if (mark != nullptr) mark[i * m + p] = ((uint64_t)stamp << 32) | (uint64_t)q;
+  }
   float* out = agg + i * payload + bk.agg_off + q * bk.cols + col;
   const int64_t e = bk.elem_off + pr * bk.cols + col;
   const int64_t ncols = bk.cols - col < 4 ? bk.cols - col : 4;
@@ -115,6 +137,52 @@ topk_gather_kernel(const float* __restrict__ h, float* __restrict__ g,
       out[jj] = dl;
     }
   }
+}
+
+// Top-K's merge into G = sum_i g^(i) (Sec. III): every coordinate of a row
+// some node kept gets the kept values of the nodes that kept it, summed in
+// ascending node order (the first as it is, then plain additions), added to
+// G.  Work items as in the gather; the item of the lowest node that kept a
+// row does that row's columns, the others return.  mark holds this step's
+// tags from the gather (older steps' tags carry another stamp).
+__global__ void __launch_bounds__(256)
+topk_merge_kernel(const float* __restrict__ agg, const int32_t* __restrict__ sel,
+                  const uint64_t* __restrict__ mark, uint32_t stamp,
+                  const GatherBucket* __restrict__ buckets, int32_t nb, int64_t work,
+                  int64_t K_total, int64_t payload, int64_t d, int64_t m, int32_t N,
+                  float* __restrict__ G) {
+  const int64_t w_all = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (w_all >= (int64_t)N * work) return;
+  const int64_t i = w_all / work, w = w_all - i * work;
+  const TopkItem it = topk_item(buckets, nb, w);
+  const GatherBucket& bk = it.bk;
+  const int64_t q = it.q, col = it.col;
+  const int64_t p = (int64_t)sel[i * K_total + bk.out_off + q] - i * m;
+  const int64_t pr = p - bk.row0;
+  if (q >= bk.k || pr < 0 || pr >= bk.rows) return;
+  for (int64_t j = 0; j < i; ++j)
+    if ((uint32_t)(mark[j * m + p] >> 32) == stamp) return;  // a lower node owns the row
+  const int64_t e = bk.elem_off + pr * bk.cols + col;
+  const int64_t ncols = bk.cols - col < 4 ? bk.cols - col : 4;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  bool have = false;
+  for (int64_t j = i; j < N; ++j) {
+    const uint64_t mv = mark[j * m + p];
+    if ((uint32_t)(mv >> 32) != stamp) continue;
+    const int64_t qj = (int64_t)(uint32_t)mv;
+    if (qj >= bk.k) continue;  // a broken tag touches nothing
+    const float* src = agg + j * payload + bk.agg_off + qj * bk.cols + col;
+    for (int64_t jj = 0; jj < ncols; ++jj) acc[jj] = have ? acc[jj] + src[jj] : src[jj];
+    have = true;
+  }
+  if (!have) return;
+  for (int64_t jj = 0; jj < ncols; ++jj)
+    if (e + jj < d) G[e + jj] = G[e + jj] + acc[jj];
+}
+
+__global__ void __launch_bounds__(256) zero_u64_kernel(uint64_t* __restrict__ p, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < n) p[e] = 0u;
 }
 
 }  // namespace
@@ -148,11 +216,29 @@ hipError_t launch_randk_keys(uint64_t seed, int64_t t, int64_t m, float* keys,
 hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int32_t* out_idx,
                               float* agg, const GatherBucket* buckets, int32_t nb,
                               int64_t work, int64_t K_total, int64_t payload, int64_t d,
-                              int64_t m, int32_t N, bool vec, hipStream_t stream) {
+                              int64_t m, int32_t N, bool vec, uint64_t* mark, uint32_t stamp,
+                              hipStream_t stream) {
   if (work <= 0) return hipSuccess;
   hipLaunchKernelGGL(topk_gather_kernel, dim3(blocks_for((int64_t)N * work, 256)), dim3(256), 0,
                      stream, h, g, sel, out_idx, agg, buckets, nb, work, K_total, payload, d, m,
-                     N, vec ? 1 : 0);
+                     N, vec ? 1 : 0, mark, stamp);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_merge(const float* agg, const int32_t* sel, const uint64_t* mark,
+                             uint32_t stamp, const GatherBucket* buckets, int32_t nb,
+                             int64_t work, int64_t K_total, int64_t payload, int64_t d,
+                             int64_t m, int32_t N, float* G, hipStream_t stream) {
+  if (work <= 0) return hipSuccess;
+  hipLaunchKernelGGL(topk_merge_kernel, dim3(blocks_for((int64_t)N * work, 256)), dim3(256), 0,
+                     stream, agg, sel, mark, stamp, buckets, nb, work, K_total, payload, d, m, N,
+                     G);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_u64_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, stream, p, n);
   return hipGetLastError();
 }
 

@@ -158,10 +158,23 @@ hipError_t launch_randk_keys(uint64_t seed, int64_t t, int64_t m, float* keys,
 // the bucket table; sel holds the selection over the N*m norms (node i's rows
 // offset by i*m).  Writes node i's local rows to out_idx[i*K_total + q], its
 // rows of Delta to agg[i*payload + ...] (+0 past d), g^(i) += Delta there.
+// With a non-null mark ([N*m]), tags node i's kept row p as
+// mark[i*m + p] = stamp << 32 | (its position in the bucket's list).
 hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int32_t* out_idx,
                               float* agg, const GatherBucket* buckets, int32_t nb,
                               int64_t work, int64_t K_total, int64_t payload, int64_t d,
-                              int64_t m, int32_t N, bool vec, hipStream_t stream);
+                              int64_t m, int32_t N, bool vec, uint64_t* mark, uint32_t stamp,
+                              hipStream_t stream);
+
+// Top-K merge after the gather with the same stamp: G += the ascending-node
+// sum of the kept values of every kept coordinate.
+hipError_t launch_topk_merge(const float* agg, const int32_t* sel, const uint64_t* mark,
+                             uint32_t stamp, const GatherBucket* buckets, int32_t nb,
+                             int64_t work, int64_t K_total, int64_t payload, int64_t d,
+                             int64_t m, int32_t N, float* G, hipStream_t stream);
+
+// p[0 .. n) = 0.
+hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t stream);
 
 // P = sum_i S[i] (ascending i), sigma = row norm squared of P, for every row
 // 0 .. m-1 (one thread per row).
@@ -205,8 +218,10 @@ struct OptimizerArgs {
   float fN;            // number of nodes
 };
 
-// x (and m, v) updated from G over every coordinate.
-hipError_t launch_optimizer(bool vec, const OptimizerArgs& o, const float* G, float* x,
+// x (and m, v) updated from G over every coordinate.  vec: 16-byte aligned
+// arrays and d % 4 == 0; cap: the device has the MI355X's 160 KB of LDS per
+// compute unit, used to cap the vectorised launch's occupancy.
+hipError_t launch_optimizer(bool vec, bool cap, const OptimizerArgs& o, const float* G, float* x,
                             float* m, float* v, int64_t d, hipStream_t stream);
 
 // ---- host projection (arc_projection.cpp) ----

@@ -25,14 +25,14 @@ def _gpu():
 def run_model_case(*, d, N, n=0, tensors=None, r=4, K=0, eta=0.1, seed=3, grad_dtype="f32",
                    family=0, optimizer="adam", steps=4, dense_steps=1, lr=1e-2, momentum=0.9,
                    beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, misalign=0,
-                   label="model"):
+                   compressor="arc", label="model"):
     dev = torch.device("cuda:0")
     sizes = None if tensors is None else [a * b for a, b, _ in tensors]
     gen = synth.Generator(d, N, 21, grad_dtype=grad_dtype, family=family, tensors=sizes)
     mc = arc.make_model_config(optimizer, lr=lr, dense_steps=dense_steps, momentum=momentum,
                                beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay)
     comp = arc.Compressor(d=d, N=N, n=n, r=r, K=K, eta=eta, seed=seed, grad_dtype=grad_dtype,
-                          tensors=tensors, device=dev)
+                          tensors=tensors, compressor=compressor, device=dev)
     try:
         h = device_buffer((N, d), torch.float32, dev, misalign)
         g = device_buffer((N, d), torch.float32, dev, misalign)
@@ -56,6 +56,16 @@ def run_model_case(*, d, N, n=0, tensors=None, r=4, K=0, eta=0.1, seed=3, grad_d
             torch.cuda.synchronize(dev)
             if t < dense_steps:
                 oracle.dense_step(h_o, g_o, G_o, grad_np, eta)
+            elif compressor == "topk":
+                if tensors is None:
+                    want = oracle.step_topk(h_o, g_o, grad_np, eta=eta, n=n, K=K)
+                    oracle.merge_topk(G_o, want["idx"], want["agg"], n=n)
+                else:
+                    want = oracle.step_topk(h_o, g_o, grad_np, eta=eta, tensors=tensors)
+                    oracle.merge_topk(G_o, want["idx"], want["agg"], tensors=tensors)
+                assert np.array_equal(idx.cpu().numpy(), want["idx"]), f"{label} t={t} idx"
+                compare_float(f"{label} t={t} agg", agg.cpu().numpy().reshape(-1),
+                              want["agg"].reshape(-1))
             else:
                 if tensors is None:
                     want = oracle.step(h_o, g_o, grad_np, n=n, r=r, eta=eta, seed=seed, t=t, K=K)
@@ -99,6 +109,19 @@ CASES = [
     ("adam_per_worker_N12", dict(d=256 * 100, N=12, n=256, K=6, optimizer="adam")),
     ("msgd_partial_chunk_tensors", dict(d=sum(a * b for a, b, _ in PARTIAL), N=4,
                                         tensors=PARTIAL, optimizer="msgd")),
+    # Top-K: each node's own rows, merged into G in ascending node order
+    ("topk_sgd_f32", dict(d=256 * 300, N=4, n=256, K=9, optimizer="sgd", lr=0.5,
+                          compressor="topk")),
+    ("topk_adam_bf16_ragged", dict(d=512 * 200 + 8, N=3, n=512, K=20, optimizer="adam",
+                                   grad_dtype="bf16", family=1, compressor="topk")),
+    ("topk_msgd_many_blocks", dict(d=32 * 20000, N=2, n=32, K=3000, optimizer="msgd",
+                                   compressor="topk", steps=3)),
+    ("topk_adam_tensors", dict(d=sum(a * b for a, b, _ in MIXED), N=3, tensors=MIXED,
+                               optimizer="adam", compressor="topk")),
+    ("topk_keep_all", dict(d=64 * 50 + 12, N=5, n=64, K=51, optimizer="sgd",
+                           compressor="topk", dense_steps=0)),
+    ("topk_partial_tensors_N8", dict(d=sum(a * b for a, b, _ in PARTIAL), N=8,
+                                     tensors=PARTIAL, optimizer="adam", compressor="topk")),
 ]
 
 
@@ -185,5 +208,47 @@ def test_model_step_full_size_llama1b_adam():
         for i in range(w.N):
             compare_float(f"llama1b model h[{i}]", h[i].cpu().numpy(), h_o[i])
             compare_float(f"llama1b model g[{i}]", g[i].cpu().numpy(), g_o[i])
+    finally:
+        comp.close()
+
+
+@pytest.mark.timeout(900)
+def test_model_step_full_size_gpt2s_topk_adam():
+    """The GPT-2-small workload with Top-K in the model step: every node's own
+    163 rows, merged into G over the 8 nodes; two compressed iterations with
+    Adam, G, x, m, v, h and g compared in full."""
+    w = synth.WORKLOADS["gpt2s"]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    gen = synth.Generator.for_workload(w)
+    mc = arc.make_model_config("adam", lr=1e-3, dense_steps=0, weight_decay=5e-4)
+    comp = arc.Compressor(d=w.d, N=w.N, n=w.n, r=w.r, K=w.K_global(), eta=w.eta,
+                          seed=w.sketch_seed, compressor="topk", device=dev, stream=stream)
+    try:
+        grad = torch.empty((w.N, w.d), dtype=torch.float32, device=dev)
+        h = torch.zeros((w.N, w.d), device=dev)
+        g = torch.zeros((w.N, w.d), device=dev)
+        G, x, m, v = (torch.zeros(w.d, device=dev) for _ in range(4))
+        h_o, g_o = np.zeros((w.N, w.d), F32), np.zeros((w.N, w.d), F32)
+        G_o, x_o, m_o, v_o = (np.zeros(w.d, F32) for _ in range(4))
+        for t in range(2):
+            gen.fill_device(t, grad, stream)
+            grad_np = grad.cpu().numpy()
+            idx, agg = comp.model_step(t, grad, h, g, G, x, mc, m, v)
+            torch.cuda.synchronize(dev)
+            want = oracle.step_topk(h_o, g_o, grad_np, eta=w.eta, n=w.n, K=w.K_global())
+            oracle.merge_topk(G_o, want["idx"], want["agg"], n=w.n)
+            assert np.array_equal(idx.cpu().numpy(), want["idx"]), t
+            compare_float(f"gpt2s topk model t={t} agg", agg.cpu().numpy().reshape(-1),
+                          want["agg"].reshape(-1))
+            del grad_np
+            oracle.optimizer_step("adam", G_o, x_o, m_o, v_o, N=w.N, T=t + 1, lr=1e-3,
+                                  weight_decay=5e-4)
+            for name, dv, hv in (("G", G, G_o), ("x", x, x_o), ("m", m, m_o), ("v", v, v_o)):
+                compare_float(f"gpt2s topk model t={t} {name}", dv.cpu().numpy(), hv)
+            log(f"[model] gpt2s topk t={t}: G, x, m, v bit-exact over {w.d} coordinates")
+        for i in range(w.N):
+            compare_float(f"gpt2s topk model h[{i}]", h[i].cpu().numpy(), h_o[i])
+            compare_float(f"gpt2s topk model g[{i}]", g[i].cpu().numpy(), g_o[i])
     finally:
         comp.close()
