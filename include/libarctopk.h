@@ -250,6 +250,37 @@ arc_status arc_model_step(arc_ctx *ctx, const arc_model_config *mc, int64_t t,
                           const void *grad, float *h, float *g, float *G, float *x,
                           float *opt_m, float *opt_v, int32_t *out_idx, float *out_agg);
 
+/*
+ * Allocation-free step, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same step as arc_create + arc_step (same kernels, same
+ * bits for every output) from a configuration, with no context.  Every
+ * device buffer the step needs beyond the caller's grad, h, g, out_idx and
+ * out_agg (the kernels' tables, V_t, the per-worker sketch, the importance,
+ * the selection's scratch) lives in one static device array of
+ * ARC_STATIC_SCRATCH_BYTES per device, which the library holds from the
+ * first call on a device until the process ends.  The call allocates no
+ * device or pinned host memory; it plans the step on the host (ordinary heap
+ * memory), generates V_t on the host and copies the tables and V_t into the
+ * static array on hip_stream, then enqueues the step there.
+ *   cfg, t, grad, h, g, out_idx, out_agg  as for arc_create and arc_step
+ *                 (out_idx [K_total], out_agg [payload]: arc_selected_rows /
+ *                 arc_payload_elems of a context of the same cfg)
+ *   hip_stream    the hipStream_t to run on (NULL = the default stream)
+ * A configuration whose buffers exceed ARC_STATIC_SCRATCH_BYTES (about
+ * 16*N*m*r + 4*m bytes plus the tables) gives ARC_ERR_INVALID, as do the
+ * invalid arguments arc_create and arc_step reject, before any device work.
+ * Every call on one device shares that device's array and leaves its
+ * contents behind: calls on one device that overlap in time (two streams,
+ * or two host threads) race and give undefined results; calls in stream
+ * order, or on one stream, are safe.  Before refilling its host copy of the
+ * tables the call waits until the device has read the previous call's.
+ */
+#define ARC_STATIC_SCRATCH_BYTES (64u * 1024u * 1024u)
+arc_status arc_step_static(const arc_config *cfg, void *hip_stream, int64_t t,
+                           const void *grad, float *h, float *g, int32_t *out_idx,
+                           float *out_agg);
+
 /* Release the context and its workspace.  NULL is accepted.  Waits for the
  * context's stream to finish its work first. */
 arc_status arc_destroy(arc_ctx *ctx);

@@ -13,7 +13,8 @@ from ._lib import (  # noqa: F401
     ARC_OPT_SGD, EXPORTED, LIB_PATH, OPTIMIZERS, STAGE_NAMES, ArcError, arc_config, arc_create,
     arc_debug_projection, arc_describe, arc_debug_sigma, arc_debug_sketch, arc_destroy,
     arc_last_error, arc_model_config, arc_model_step, arc_num_rows, arc_payload_elems,
-    arc_projection, arc_selected_rows, arc_set_projection, arc_status_str, arc_step, arc_tensor,
+    arc_projection, arc_selected_rows, arc_set_projection, arc_status_str, arc_step,
+    arc_step_static, ARC_STATIC_SCRATCH_BYTES, arc_tensor,
     arc_timing_enable, arc_timing_read, make_config, make_model_config)
 
 

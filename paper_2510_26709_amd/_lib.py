@@ -32,6 +32,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 ARC_OK, ARC_ERR_INVALID, ARC_ERR_NOMEM, ARC_ERR_DEVICE, ARC_ERR_UNSUPPORTED = 0, 1, 2, 3, 4
 ARC_DTYPE_F32, ARC_DTYPE_BF16 = 0, 1
 ARC_MAX_R = 32
+ARC_STATIC_SCRATCH_BYTES = 64 * 1024 * 1024
 ARC_NUM_STAGES = 5
 STAGE_NAMES = ("sketch", "reduce", "select", "gather_update", "step")
 
@@ -96,6 +97,8 @@ _SIGS = {
     "arc_step": (_st, [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp]),
     "arc_model_step": (_st, [_vp, ctypes.POINTER(arc_model_config), ctypes.c_int64, _vp, _vp,
                              _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "arc_step_static": (_st, [ctypes.POINTER(arc_config), _vp, ctypes.c_int64, _vp, _vp, _vp,
+                              _vp, _vp]),
     "arc_destroy": (_st, [_vp]),
     "arc_num_rows": (ctypes.c_int64, [_vp]),
     "arc_selected_rows": (ctypes.c_int64, [_vp]),
@@ -186,6 +189,15 @@ def arc_create(cfg: arc_config, hip_stream=None) -> int:
 def arc_step(ctx: int, t: int, grad, h, g, out_idx, out_agg) -> None:
     _check(_lib.arc_step(ctx, t, _addr(grad), _addr(h), _addr(g), _addr(out_idx),
                          _addr(out_agg)), "arc_step")
+
+
+def arc_step_static(cfg: arc_config, stream, t: int, grad, h, g, out_idx, out_agg) -> None:
+    """The allocation-free step: no context, device scratch in the library's
+    static array.  stream: a torch stream, a raw hipStream_t or None."""
+    _check(_lib.arc_step_static(ctypes.byref(cfg), getattr(stream, "cuda_stream", stream), t,
+                                _addr(grad),
+                                _addr(h), _addr(g), _addr(out_idx), _addr(out_agg)),
+           "arc_step_static")
 
 
 def arc_model_step(ctx: int, mc: arc_model_config, t: int, grad, h, g, G, x, opt_m, opt_v,

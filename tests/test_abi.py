@@ -214,3 +214,21 @@ def test_model_step_rejects_null_context_and_config():
         arc.ARC_ERR_INVALID
     assert L.arc_model_step(12345, None, 0, 1, 2, 3, 4, 5, None, None, 6, 7) == \
         arc.ARC_ERR_INVALID
+
+
+def test_static_step_rejects_before_any_device_work():
+    """arc_step_static checks the configuration and sizes its static device
+    scratch on the host: an invalid configuration, and one whose buffers
+    exceed ARC_STATIC_SCRATCH_BYTES, are rejected with no HIP call (this runs
+    without a GPU)."""
+    L = _lib._lib
+    assert L.arc_step_static(None, None, 0, 1, 2, 3, 4, 5) == arc.ARC_ERR_INVALID
+    cfg, keep = arc.make_config(**dict(BASE, r=0))
+    assert L.arc_step_static(ctypes.byref(cfg), None, 0, 1, 2, 3, 4, 5) == arc.ARC_ERR_INVALID
+    # 2^24 rows of 4 values, r = 4: a 256 MiB per-worker sketch
+    cfg, keep = arc.make_config(d=1 << 26, N=1, n=4, r=4, K=1, eta=0.1, seed=1)
+    assert L.arc_step_static(ctypes.byref(cfg), None, 0, 1, 2, 3, 4, 5) == arc.ARC_ERR_INVALID
+    msg = arc.arc_last_error()
+    assert "static" in msg and str(arc.ARC_STATIC_SCRATCH_BYTES) in msg, msg
+    with pytest.raises(arc.ArcError, match="static"):
+        arc.arc_step_static(cfg, None, 0, 1, 2, 3, 4, 5)
