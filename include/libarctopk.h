@@ -181,10 +181,11 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  * with identical results.
  * The call returns once the work is queued on the context's stream.  On the
  * host it generates V_t (ARC_COMP_ARC; V_{t+1} is then prepared in the
- * background for the next call) and waits until the device has copied in
- * the projection staged by the previous call (the first work of the
- * previous step), so it cannot be captured into a HIP graph, and the host
- * runs at most about one step ahead of the device.
+ * background for the next call) into one of four pinned staging buffers
+ * used in turn, waiting only until the device has copied in the projection
+ * staged three calls earlier (the first work of that step): the host can
+ * queue up to three steps ahead of the device.  The host work makes the
+ * call unsuitable for capture into a HIP graph.
  * On rows longer than the streaming kernel's column chunk (32 to 256
  * values, by how many rows it streams together), its workgroups each hold
  * just over half of a compute unit's LDS, so that one runs per compute

@@ -453,12 +453,14 @@ arc_status release_slot(arc_ctx* c, int s) {
 }
 
 // Pinned staging + async copy of this step's projections.  After the copy
-// is queued, the pool starts on V_{t+1} in the other slot, so that a caller
-// stepping t, t+1, ... finds the next projection ready; any other t is
-// generated on the spot.
+// is queued, the pool starts on V_{t+1} in the next slot of the ring, so
+// that a caller stepping t, t+1, ... finds the next projection ready; any
+// other t is generated on the spot.  A slot is refilled only after the copy
+// that last read it (kProjectionSlots - 1 calls earlier) has completed.
 arc_status upload_projection(arc_ctx* c, int64_t t) {
   const int s = c->V_slot;
-  c->V_slot ^= 1;
+  const int next = (s + 1) % arc::kProjectionSlots;
+  c->V_slot = next;
   c->V_pool->wait();
   const bool ready = !c->use_override && c->V_prefetch_t == t;
   c->V_prefetch_t = -1;
@@ -478,8 +480,8 @@ arc_status upload_projection(arc_ctx* c, int64_t t) {
   ARC_HIP(hipEventRecord(c->V_done[s], c->stream), "hipEventRecord(projection)");
   c->V_pending[s] = true;
   if (!c->use_override && t < INT64_MAX) {
-    if ((st = release_slot(c, s ^ 1))) return st;
-    c->V_pool->start(c->seed, t + 1, c->r, &c->V_blocks, c->V_pinned[s ^ 1]);
+    if ((st = release_slot(c, next))) return st;
+    c->V_pool->start(c->seed, t + 1, c->r, &c->V_blocks, c->V_pinned[next]);
     c->V_prefetch_t = t + 1;
   }
   return ARC_OK;
@@ -552,7 +554,7 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
                       c->compressor == ARC_COMP_TOPK ? static_cast<size_t>(c->N) * c->m : 0,
                       "hipMalloc(merge tags)")))
     return bail(st);
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < arc::kProjectionSlots; ++s) {
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
                       static_cast<size_t>(c->v_floats) * sizeof(float), hipHostMallocDefault);
     if (e != hipSuccess) {

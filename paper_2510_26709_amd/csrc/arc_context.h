@@ -21,6 +21,11 @@ namespace arc {
 // HIP events recorded per step when stage timing is on.
 constexpr int kEventsPerStep = 6;
 
+// Pinned host buffers staging V_t, used in turn: a step refills a buffer only
+// once the device has copied it in, so the host can queue this many steps
+// minus one ahead of the device before it waits.
+constexpr int kProjectionSlots = 4;
+
 // Record `why` as the calling thread's last error and return s.
 arc_status fail(arc_status s, const std::string& why);
 // The same for a HIP error at `where` (ARC_ERR_NOMEM for out-of-memory).
@@ -85,11 +90,11 @@ struct arc_ctx {
   arc::BucketState* state_dev = nullptr;
   uint32_t* hist_dev = nullptr;
   uint32_t* blockcnt_dev = nullptr;
-  // projection staging: two pinned buffers, reused every other step; the
-  // pool fills the next step's buffer while the device runs this step
-  float* V_pinned[2] = {nullptr, nullptr};
-  hipEvent_t V_done[2] = {nullptr, nullptr};
-  bool V_pending[2] = {false, false};
+  // projection staging: a ring of pinned buffers; the pool fills the next
+  // step's buffer while the device runs this step
+  float* V_pinned[arc::kProjectionSlots] = {};
+  hipEvent_t V_done[arc::kProjectionSlots] = {};
+  bool V_pending[arc::kProjectionSlots] = {};
   int V_slot = 0;
   std::vector<float> V_override;
   bool use_override = false;
@@ -140,7 +145,7 @@ struct arc_ctx {
                     static_cast<void*>(blocks_dev), static_cast<void*>(state_dev),
                     static_cast<void*>(hist_dev), static_cast<void*>(blockcnt_dev)})
       if (p) (void)hipFree(p);
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < arc::kProjectionSlots; ++s) {
       if (V_done[s]) (void)hipEventDestroy(V_done[s]);
       if (V_pinned[s]) (void)hipHostFree(V_pinned[s]);
     }

@@ -161,7 +161,7 @@ def test_workload_gpt2s_per_tensor():
 
 @pytest.mark.timeout(900)
 def test_workload_llama1b_per_tensor():
-    run_workload("llama1b_tensors", steps=4)
+    run_workload("llama1b_tensors")
 
 
 @pytest.mark.timeout(1200)
