@@ -182,7 +182,7 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  * The call returns once the work is queued on the context's stream.  On the
  * host it generates V_t (ARC_COMP_ARC; V_{t+1} is then prepared in the
  * background for the next call) into one of four pinned staging buffers
- * used in turn, waiting only until the device has copied in the projection
+ * used in turn, waiting only until the device has read the projection
  * staged three calls earlier (the first work of that step): the host can
  * queue up to three steps ahead of the device.  The host work makes the
  * call unsuitable for capture into a HIP graph.

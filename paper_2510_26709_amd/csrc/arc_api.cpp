@@ -474,9 +474,12 @@ arc_status upload_projection(arc_ctx* c, int64_t t) {
       c->V_pool->wait();
     }
   }
-  ARC_HIP(hipMemcpyAsync(c->V_dev, c->V_pinned[s], static_cast<size_t>(c->v_floats) * sizeof(float),
-                         hipMemcpyHostToDevice, c->stream),
-          "hipMemcpyAsync(projection)");
+  // A kernel reads the pinned buffer through its device mapping: with the
+  // host queueing steps ahead, the runtime's copy of a pinned buffer stalled
+  // the calling thread for 11-12 ms every eighth or ninth step (per-tensor
+  // ResNet-18, four buffers in the ring), which this does not.
+  ARC_HIP(arc::launch_stage_projection(c->V_pinned_dev[s], c->V_dev, c->v_floats, c->stream),
+          "projection staging launch");
   ARC_HIP(hipEventRecord(c->V_done[s], c->stream), "hipEventRecord(projection)");
   c->V_pending[s] = true;
   if (!c->use_override && t < INT64_MAX) {
@@ -555,12 +558,17 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
                       "hipMalloc(merge tags)")))
     return bail(st);
   for (int s = 0; s < arc::kProjectionSlots; ++s) {
+    // Coherent and mapped: the staging kernel reads it from the device, and
+    // every step rewrites it, so the device must not keep stale copies.
     e = hipHostMalloc(reinterpret_cast<void**>(&c->V_pinned[s]),
-                      static_cast<size_t>(c->v_floats) * sizeof(float), hipHostMallocDefault);
+                      static_cast<size_t>(std::max<int64_t>(c->v_floats, 1)) * sizeof(float),
+                      hipHostMallocMapped | hipHostMallocCoherent);
     if (e != hipSuccess) {
       c->V_pinned[s] = nullptr;
       return bail(fail_hip(e, "hipHostMalloc(projection)"));
     }
+    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->V_pinned_dev[s]), c->V_pinned[s], 0);
+    if (e != hipSuccess) return bail(fail_hip(e, "hipHostGetDevicePointer(projection)"));
     e = hipEventCreateWithFlags(&c->V_done[s], hipEventDisableTiming);
     if (e != hipSuccess) {
       c->V_done[s] = nullptr;
@@ -580,8 +588,10 @@ arc_status arc_create(const arc_config* cfg, void* hip_stream, arc_ctx** out) {
     for (int sz = 0; sz < 4; ++sz) launches += c->vec_count[sz] > 0;
     if (launches > 1) {
       e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
-      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->fork_ev, hipEventDisableTiming);
-      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming);
+      for (int k = 0; k < arc::kProjectionSlots && e == hipSuccess; ++k) {
+        e = hipEventCreateWithFlags(&c->fork_ev[k], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->join_ev[k], hipEventDisableTiming);
+      }
       if (e != hipSuccess) return bail(fail_hip(e, "hipStreamCreate(side)"));
     }
   }
@@ -672,8 +682,9 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
     if (elems(which[l]) > elems(which[big])) big = l;
   const bool fork = nl > 1 && c->side != nullptr;
   if (fork) {
-    ARC_HIP(hipEventRecord(c->fork_ev, c->stream), "hipEventRecord(fork)");
-    ARC_HIP(hipStreamWaitEvent(c->side, c->fork_ev, 0), "hipStreamWaitEvent(fork)");
+    c->fork_slot = (c->fork_slot + 1) % arc::kProjectionSlots;
+    ARC_HIP(hipEventRecord(c->fork_ev[c->fork_slot], c->stream), "hipEventRecord(fork)");
+    ARC_HIP(hipStreamWaitEvent(c->side, c->fork_ev[c->fork_slot], 0), "hipStreamWaitEvent(fork)");
   }
   // The smaller launches go first, so that they start while the largest
   // fills the rest of the device.
@@ -707,8 +718,8 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
     }
   }
   if (fork) {
-    ARC_HIP(hipEventRecord(c->join_ev, c->side), "hipEventRecord(join)");
-    ARC_HIP(hipStreamWaitEvent(c->stream, c->join_ev, 0), "hipStreamWaitEvent(join)");
+    ARC_HIP(hipEventRecord(c->join_ev[c->fork_slot], c->side), "hipEventRecord(join)");
+    ARC_HIP(hipStreamWaitEvent(c->stream, c->join_ev[c->fork_slot], 0), "hipStreamWaitEvent(join)");
   }
   return ARC_OK;
 }

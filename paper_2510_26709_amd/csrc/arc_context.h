@@ -71,7 +71,10 @@ struct arc_ctx {
   // second stream for the smaller launches of the streaming stage, forked
   // from and joined back into `stream` (only when there are several)
   hipStream_t side = nullptr;
-  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
+  // a pair of events per step in flight, used in turn (an event is
+  // re-recorded only after kProjectionSlots further steps)
+  hipEvent_t fork_ev[arc::kProjectionSlots] = {}, join_ev[arc::kProjectionSlots] = {};
+  int fork_slot = 0;
   int device = 0;
   size_t max_lds_per_block = 0;
   int lds_per_cu = 0;
@@ -93,6 +96,7 @@ struct arc_ctx {
   // projection staging: a ring of pinned buffers; the pool fills the next
   // step's buffer while the device runs this step
   float* V_pinned[arc::kProjectionSlots] = {};
+  float* V_pinned_dev[arc::kProjectionSlots] = {};  // the same buffers, device-mapped
   hipEvent_t V_done[arc::kProjectionSlots] = {};
   bool V_pending[arc::kProjectionSlots] = {};
   int V_slot = 0;
@@ -136,8 +140,9 @@ struct arc_ctx {
       (void)hipStreamSynchronize(side);
       (void)hipStreamDestroy(side);
     }
-    for (hipEvent_t e : {fork_ev, join_ev})
-      if (e) (void)hipEventDestroy(e);
+    for (int k = 0; k < arc::kProjectionSlots; ++k)
+      for (hipEvent_t e : {fork_ev[k], join_ev[k]})
+        if (e) (void)hipEventDestroy(e);
     for (void* p : {static_cast<void*>(V_dev), static_cast<void*>(S_dev),
                     static_cast<void*>(sigma_dev), static_cast<void*>(groups_dev),
                     static_cast<void*>(sel_dev), static_cast<void*>(mark_dev),

@@ -176,6 +176,10 @@ hipError_t launch_topk_merge(const float* agg, const int32_t* sel, const uint64_
 // p[0 .. n) = 0.
 hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t stream);
 
+// dst[0 .. n) = src[0 .. n), src a device mapping of pinned host memory (the
+// projection staging buffer of one step).
+hipError_t launch_stage_projection(const float* src, float* dst, int64_t n, hipStream_t stream);
+
 // P = sum_i S[i] (ascending i), sigma = row norm squared of P, for every row
 // 0 .. m-1 (one thread per row).
 hipError_t launch_reduce_rows(const float* S, float* sigma, int64_t m, int32_t N, int32_t r,
