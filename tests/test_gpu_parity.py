@@ -341,3 +341,53 @@ def test_two_contexts_on_two_streams_interleaved():
     finally:
         for comp in comps:
             comp.close()
+
+
+@pytest.mark.parametrize("tensors", [False, True], ids=["single_view", "tensors"])
+def test_steps_queued_ahead_of_a_busy_device(tensors):
+    # The host queues many steps while the device is still busy with earlier
+    # work, so every staging buffer of the projection ring is refilled while
+    # earlier steps are in flight (and, out of order, generated on the spot):
+    # every step must still use its own V_t.
+    from parity_util import compare_float, to_device_grad
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream(dev)
+    if tensors:
+        kw = dict(d=sum(a * b for a, b, _ in TENSORS_3W), N=3, tensors=TENSORS_3W)
+    else:
+        kw = dict(d=512 * 400 + 8, N=3, n=512, K=9)
+    ts = [0, 1, 2, 3, 4, 5, 9, 10, 11, 12, 4, 13, 14]
+    gen = synth.Generator(kw["d"], kw["N"], 41,
+                          tensors=None if not tensors else [a * b for a, b, _ in TENSORS_3W])
+    grads = [gen.fill_host(t) for t in range(len(ts))]
+    comp = arc.Compressor(r=4, eta=0.1, seed=12, device=dev, stream=stream, **kw)
+    try:
+        dgrads = [to_device_grad(x, dev) for x in grads]
+        h = torch.zeros((kw["N"], kw["d"]), device=dev)
+        g = torch.zeros((kw["N"], kw["d"]), device=dev)
+        big = torch.randn(4096, 4096, device=dev)
+        torch.cuda.synchronize(dev)
+        outs = []
+        with torch.cuda.stream(stream):
+            for _ in range(8):  # keep the device busy while the host queues the steps
+                big = big @ big * (1.0 / 64.0)
+            for k, t in enumerate(ts):
+                idx, agg = comp.step(t, dgrads[k], h, g)
+                outs.append((idx.clone(), agg.clone()))
+        torch.cuda.synchronize(dev)
+        h_o = np.zeros((kw["N"], kw["d"]), F32)
+        g_o = np.zeros((kw["N"], kw["d"]), F32)
+        for k, t in enumerate(ts):
+            if tensors:
+                want = oracle.step_tensors(h_o, g_o, grads[k], TENSORS_3W, r=4, eta=0.1, seed=12,
+                                           t=t)
+            else:
+                want = oracle.step(h_o, g_o, grads[k], n=kw["n"], r=4, eta=0.1, seed=12, t=t,
+                                   K=kw["K"])
+            assert np.array_equal(outs[k][0].cpu().numpy(), want["idx"]), (k, t)
+            compare_float(f"queued t={t} agg", outs[k][1].cpu().numpy(), want["agg"])
+        compare_float("queued h", h.cpu().numpy(), h_o)
+        compare_float("queued g", g.cpu().numpy(), g_o)
+    finally:
+        comp.close()
