@@ -39,7 +39,7 @@ class Pair:
             d=self.d, N=self.N, n=kw.get("n", 0), r=kw.get("r", 4), K=kw.get("K", 0),
             eta=kw["eta"], seed=kw["seed"],
             grad_dtype=arc.ARC_DTYPE_BF16 if grad_dtype == "bf16" else arc.ARC_DTYPE_F32,
-            buckets=kw.get("buckets"), tensors=tensors)
+            buckets=kw.get("buckets"), tensors=tensors, compressor=kw.get("compressor", "arc"))
         z = lambda: torch.zeros((self.N, self.d), dtype=torch.float32, device="cuda:0")
         self.h_ref, self.g_ref, self.h_st, self.g_st = z(), z(), z(), z()
         self.idx = torch.full((self.comp.K_total,), -1, dtype=torch.int32, device="cuda:0")
@@ -54,7 +54,7 @@ class Pair:
             arc.arc_step_static(self.cfg, self.stream, t, grad, self.h_st, self.g_st, self.idx,
                                 self.agg)
         self.stream.synchronize()
-        assert np.array_equal(self.idx.cpu().numpy(), idx_ref.cpu().numpy()), label
+        assert np.array_equal(self.idx.cpu().numpy(), idx_ref.reshape(-1).cpu().numpy()), label
         compare_float(f"{label} agg", self.agg.cpu().numpy(),
                       agg_ref.reshape(-1).cpu().numpy(), True)
         compare_float(f"{label} h", self.h_st.cpu().numpy(), self.h_ref.cpu().numpy(), True)
@@ -92,6 +92,22 @@ def test_static_step_tensors_and_buckets():
     try:
         for t in range(2):
             for p, label in zip(pairs, ("tensors", "buckets")):
+                p.step_and_compare(t, label)
+    finally:
+        for p in pairs:
+            p.close()
+
+
+def test_static_step_comparison_compressors():
+    # Rand-K (shared random rows) and Top-K (every node's own rows, over the
+    # N*m row norms): the same static array, different scratch in it.
+    stream = torch.cuda.Stream()
+    pairs = [Pair(dict(BIG, compressor="topk"), stream, 105),
+             Pair(dict(SMALL, compressor="randk"), stream, 106),
+             Pair(dict(TENSORS, compressor="topk"), stream, 107)]
+    try:
+        for t in range(2):
+            for p, label in zip(pairs, ("topk", "randk", "topk_tensors")):
                 p.step_and_compare(t, label)
     finally:
         for p in pairs:
