@@ -154,7 +154,9 @@ typedef struct {
  * importance, selection scratch) on the current HIP device and bind the
  * context to `hip_stream` (a hipStream_t; NULL = the default stream).
  * On failure *out is set to NULL.  Workspace bytes are about
- * 4*(n*r + N*m*r + 3*m) plus a few kilobytes per bucket.
+ * 4*(n*r + N*m*r + 3*m) plus a few kilobytes per bucket, and for
+ * ARC_COMP_TOPK another 8*N*m (the rows each node kept, for the merge of the
+ * model step) plus 4*N*K; pinned host memory 16*n*r.
  */
 arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
 

@@ -343,9 +343,10 @@ void launch_per_worker_waves(bool one_per_cu, const void* grad, float* h, const 
   // per-tensor ResNet-18 and tiny within 0.5%, interleaved runs on one
   // box).  With 4 workers an eighth is half a worker, and the 1.1B workload
   // read 10.2-10.3 ms against 9.5-10.0 ms with a grid row per worker, which
-  // other worker counts therefore keep.
-  const bool flat = N % 8 == 0;
+  // other worker counts therefore keep (as does a grid too large for one
+  // dimension).
   const unsigned nbx = blocks_for(ngroups, WAVES);
+  const bool flat = N % 8 == 0 && (int64_t)nbx * N <= INT32_MAX;
   hipLaunchKernelGGL((sketch_per_worker_kernel<R, BF16, G, WAVES, NORM>),
                      flat ? dim3(nbx * (unsigned)N) : dim3(nbx, (unsigned)N), dim3(WAVES * kWave),
                      reserve, stream, grad, h, g, V, groups, ngroups, S, d, m, eta, a,

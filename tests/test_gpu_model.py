@@ -122,6 +122,8 @@ CASES = [
                            compressor="topk", dense_steps=0)),
     ("topk_partial_tensors_N8", dict(d=sum(a * b for a, b, _ in PARTIAL), N=8,
                                      tensors=PARTIAL, optimizer="adam", compressor="topk")),
+    ("topk_general_n100", dict(d=100 * 321 + 7, N=3, n=100, K=12, optimizer="adam",
+                               compressor="topk")),
 ]
 
 
@@ -131,10 +133,11 @@ def test_model_step_parity(name, kw):
     run_model_case(label=name, **kw)
 
 
-def test_model_step_misaligned_pointers():
-    log("[model] misaligned")
-    run_model_case(label="model_misaligned", d=256 * 80, N=3, n=256, K=5, optimizer="adam",
-                   misalign=1, dense_steps=1, steps=3)
+@pytest.mark.parametrize("compressor", ["arc", "topk"])
+def test_model_step_misaligned_pointers(compressor):
+    log(f"[model] misaligned {compressor}")
+    run_model_case(label=f"model_misaligned_{compressor}", d=256 * 80, N=3, n=256, K=5,
+                   optimizer="adam", misalign=1, dense_steps=1, steps=3, compressor=compressor)
 
 
 def test_model_step_rejects_bad_settings():

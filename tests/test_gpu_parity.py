@@ -50,6 +50,11 @@ CASES = [
     ("bf16_r8_N2", dict(d=64 * 3000, N=2, n=64, r=8, K=40, steps=2, grad_dtype="bf16",
                               family=1)),
     ("select_many_blocks", dict(d=32 * 300_000, N=1, n=32, r=4, K=150_000, steps=1)),
+    # worker counts that are multiples of 8 take the one-dimensional
+    # (worker, block) grid
+    ("flat_grid_N16", dict(d=768 * 400 + 16, N=16, n=768, r=4, K=6, steps=2)),
+    ("flat_grid_N24_bf16", dict(d=2048 * 90, N=24, n=2048, r=4, K=4, steps=2,
+                                grad_dtype="bf16", family=1)),
     ("generic_r32_max", dict(d=40 * 500 + 13, N=3, n=40, r=32, K=7, steps=2)),
     ("generic_r17_bf16", dict(d=72 * 300 + 5, N=2, n=72, r=17, K=9, steps=2, grad_dtype="bf16",
                               family=1)),
