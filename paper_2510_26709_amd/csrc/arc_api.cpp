@@ -118,8 +118,14 @@ arc_status check_tensors(const arc_config* cfg, int64_t* m_out) {
   return ARC_OK;
 }
 
-// Configuration checks shared by arc_create; no HIP call is made here.
-arc_status check_config_impl(const arc_config* cfg, int64_t* m_out) {
+}  // namespace
+
+namespace arc {
+
+namespace {
+
+// The checks of everything but the compressor's own bounds.
+arc_status check_problem(const arc_config* cfg, int64_t* m_out) {
   if (cfg == nullptr) return fail(ARC_ERR_INVALID, "cfg is NULL");
   if (cfg->d <= 0) return fail(ARC_ERR_INVALID, "d must be > 0");
   if (cfg->N <= 0 || cfg->N > 65535) return fail(ARC_ERR_INVALID, "N must be in 1..65535");
@@ -154,6 +160,21 @@ arc_status check_config_impl(const arc_config* cfg, int64_t* m_out) {
   *m_out = m;
   return ARC_OK;
 }
+
+}  // namespace
+
+// Configuration checks shared by the entry points; no HIP call is made here.
+arc_status check_config(const arc_config* cfg, int64_t* m_out) {
+  const arc_status st = check_problem(cfg, m_out);
+  if (st != ARC_OK) return st;
+  if (cfg->compressor == ARC_COMP_TOPK && *m_out > INT32_MAX / cfg->N)
+    return fail(ARC_ERR_INVALID, "Top-K: N * m must be below 2^31");
+  return ARC_OK;
+}
+
+}  // namespace arc
+
+namespace {
 
 // Selection buckets from row boundaries begin[0..nb] and requested K's.
 // Fat blocks (few blocks per bucket keep the per-bin atomics and the
@@ -626,10 +647,10 @@ int64_t arc_payload_elems(const arc_ctx* ctx) { return ctx ? ctx->payload : -1; 
 
 }  // extern "C"
 
-namespace {
+namespace arc {
 
 // need_outputs: the call writes out_idx / out_agg (every compressed step).
-arc_status check_step_args_impl(const arc_ctx* c, int64_t t, const void* grad, const float* h,
+arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const float* h,
                            const float* g, const int32_t* out_idx, const float* out_agg,
                            bool need_outputs) {
   if (c == nullptr) return fail(ARC_ERR_INVALID, "ctx is NULL");
@@ -661,6 +682,10 @@ arc_status check_step_args_impl(const arc_ctx* c, int64_t t, const void* grad, c
   }
   return ARC_OK;
 }
+
+}  // namespace arc
+
+namespace {
 
 // The streaming stage (S1-S3; norm: Top-K's row norms): one launch per
 // row-group size present and one for the general groups.  When there are several, the one over the most coordinates runs on
@@ -724,10 +749,14 @@ arc_status launch_streaming_stage(arc_ctx* c, const void* grad, float* h, const 
   return ARC_OK;
 }
 
+}  // namespace
+
+namespace arc {
+
 // The compressor step (arguments already checked); with a non-null G the
 // payload is also added into G at the selected coordinates.
-arc_status enqueue_step_impl(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
-                             int32_t* out_idx, float* out_agg, float* G) {
+arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
+                        int32_t* out_idx, float* out_agg, float* G) {
   // Vectorisable groups take the 16-byte kernels only when the three streams
   // are 16-byte aligned; otherwise every group takes the general kernel.
   const int64_t ngroups = static_cast<int64_t>(c->groups.size());
@@ -826,6 +855,10 @@ arc_status enqueue_step_impl(arc_ctx* c, int64_t t, const void* grad, float* h, 
   if ((st = record(c, slot, 5))) return st;
   return ARC_OK;
 }
+
+}  // namespace arc
+
+namespace {
 
 bool finite(float v) { return std::isfinite(v); }
 
@@ -1033,14 +1066,6 @@ arc_status arc_timing_read(arc_ctx* c, double* ms, int64_t* steps) {
 
 namespace arc {
 
-arc_status check_config(const arc_config* cfg, int64_t* m_out) {
-  const arc_status st = check_config_impl(cfg, m_out);
-  if (st != ARC_OK) return st;
-  if (cfg->compressor == ARC_COMP_TOPK && *m_out > INT32_MAX / cfg->N)
-    return fail(ARC_ERR_INVALID, "Top-K: N * m must be below 2^31");
-  return ARC_OK;
-}
-
 arc_status plan_context(const arc_config* cfg, int64_t m, void* stream, arc_ctx* c) {
   try {
     c->d = cfg->d;
@@ -1078,17 +1103,6 @@ arc_status bind_device(arc_ctx* c) {
   if (lds_cu != kLdsPerCu || lds_limit < kLdsPerCu / 2 + 1024)
     for (auto& o : c->vec_occ) o.one_per_cu = 0;
   return ARC_OK;
-}
-
-arc_status check_step_args(const arc_ctx* c, int64_t t, const void* grad, const float* h,
-                           const float* g, const int32_t* out_idx, const float* out_agg,
-                           bool need_outputs) {
-  return check_step_args_impl(c, t, grad, h, g, out_idx, out_agg, need_outputs);
-}
-
-arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float* g,
-                        int32_t* out_idx, float* out_agg, float* G) {
-  return enqueue_step_impl(c, t, grad, h, g, out_idx, out_agg, G);
 }
 
 }  // namespace arc
