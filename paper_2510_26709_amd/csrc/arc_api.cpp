@@ -817,7 +817,7 @@ arc_status enqueue_step(arc_ctx* c, int64_t t, const void* grad, float* h, float
       ARC_HIP(arc::launch_topk_merge(out_agg, c->sel_dev, c->mark_dev, c->mark_stamp,
                                      c->gather_dev, static_cast<int32_t>(c->gather.size()),
                                      c->gather_work, c->K_node, c->payload_node, c->d, c->m,
-                                     c->N, G, c->stream),
+                                     c->N, G, vec && aligned16(G), c->stream),
               "merge launch");
     return record(c, slot, 5);
   } else {

@@ -150,7 +150,7 @@ topk_merge_kernel(const float* __restrict__ agg, const int32_t* __restrict__ sel
                   const uint64_t* __restrict__ mark, uint32_t stamp,
                   const GatherBucket* __restrict__ buckets, int32_t nb, int64_t work,
                   int64_t K_total, int64_t payload, int64_t d, int64_t m, int32_t N,
-                  float* __restrict__ G) {
+                  float* __restrict__ G, int32_t vec) {
   const int64_t w_all = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (w_all >= (int64_t)N * work) return;
   const int64_t i = w_all / work, w = w_all - i * work;
@@ -164,6 +164,37 @@ topk_merge_kernel(const float* __restrict__ agg, const int32_t* __restrict__ sel
     if ((uint32_t)(mark[j * m + p] >> 32) == stamp) return;  // a lower node owns the row
   const int64_t e = bk.elem_off + pr * bk.cols + col;
   const int64_t ncols = bk.cols - col < 4 ? bk.cols - col : 4;
+  if (vec && bk.vec && e + 4 <= d) {
+    // four columns as one 16-byte access each (rows, payload slots and G
+    // 16-byte aligned)
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    bool have = false;
+    for (int64_t j = i; j < N; ++j) {
+      const uint64_t mv = mark[j * m + p];
+      if ((uint32_t)(mv >> 32) != stamp) continue;
+      const int64_t qj = (int64_t)(uint32_t)mv;
+      if (qj >= bk.k) continue;  // a broken tag touches nothing
+      const float4 v = *reinterpret_cast<const float4*>(agg + j * payload + bk.agg_off +
+                                                        qj * bk.cols + col);
+      if (have) {
+        acc.x = acc.x + v.x;
+        acc.y = acc.y + v.y;
+        acc.z = acc.z + v.z;
+        acc.w = acc.w + v.w;
+      } else {
+        acc = v;
+      }
+      have = true;
+    }
+    if (!have) return;
+    float4 Gv = *reinterpret_cast<const float4*>(G + e);
+    Gv.x = Gv.x + acc.x;
+    Gv.y = Gv.y + acc.y;
+    Gv.z = Gv.z + acc.z;
+    Gv.w = Gv.w + acc.w;
+    *reinterpret_cast<float4*>(G + e) = Gv;
+    return;
+  }
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   bool have = false;
   for (int64_t j = i; j < N; ++j) {
@@ -228,11 +259,11 @@ hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int3
 hipError_t launch_topk_merge(const float* agg, const int32_t* sel, const uint64_t* mark,
                              uint32_t stamp, const GatherBucket* buckets, int32_t nb,
                              int64_t work, int64_t K_total, int64_t payload, int64_t d,
-                             int64_t m, int32_t N, float* G, hipStream_t stream) {
+                             int64_t m, int32_t N, float* G, bool vec, hipStream_t stream) {
   if (work <= 0) return hipSuccess;
   hipLaunchKernelGGL(topk_merge_kernel, dim3(blocks_for((int64_t)N * work, 256)), dim3(256), 0,
                      stream, agg, sel, mark, stamp, buckets, nb, work, K_total, payload, d, m, N,
-                     G);
+                     G, vec ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -167,11 +167,12 @@ hipError_t launch_topk_gather(const float* h, float* g, const int32_t* sel, int3
                               hipStream_t stream);
 
 // Top-K merge after the gather with the same stamp: G += the ascending-node
-// sum of the kept values of every kept coordinate.
+// sum of the kept values of every kept coordinate.  vec: the gather's
+// 16-byte condition holds and G is 16-byte aligned.
 hipError_t launch_topk_merge(const float* agg, const int32_t* sel, const uint64_t* mark,
                              uint32_t stamp, const GatherBucket* buckets, int32_t nb,
                              int64_t work, int64_t K_total, int64_t payload, int64_t d,
-                             int64_t m, int32_t N, float* G, hipStream_t stream);
+                             int64_t m, int32_t N, float* G, bool vec, hipStream_t stream);
 
 // p[0 .. n) = 0.
 hipError_t launch_zero_u64(uint64_t* p, int64_t n, hipStream_t stream);
