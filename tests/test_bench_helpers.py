@@ -77,3 +77,17 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one MI355X" in r.stderr
+
+
+def test_host_info_states_cores_and_memory():
+    info = bench.host_info()
+    assert info["nproc"] == os.cpu_count()
+    assert 1 <= info.get("affinity_cpus", 1) <= info["nproc"]
+    assert 0 < info["mem_available_GB"] <= info["mem_total_GB"]
+
+
+def test_unknown_workloads_are_refused():
+    for args in (["--workload", "nope"], ["--also", "gpt2s,nope"]):
+        r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args],
+                           capture_output=True, text=True, timeout=120)
+        assert r.returncode == 2 and "unknown workload" in r.stderr, r.stderr
