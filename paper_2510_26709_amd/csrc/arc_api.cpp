@@ -464,7 +464,8 @@ int projection_threads(int64_t v_floats) {
   return static_cast<int>(std::min(by_size, cap));
 }
 
-// Waits until the device has read pinned slot s (its last copy is done).
+// Waits until the device has read pinned slot s (its last staging kernel is
+// done).
 arc_status release_slot(arc_ctx* c, int s) {
   if (c->V_pending[s]) {
     ARC_HIP(hipEventSynchronize(c->V_done[s]), "hipEventSynchronize(projection)");
@@ -473,11 +474,12 @@ arc_status release_slot(arc_ctx* c, int s) {
   return ARC_OK;
 }
 
-// Pinned staging + async copy of this step's projections.  After the copy
-// is queued, the pool starts on V_{t+1} in the next slot of the ring, so
-// that a caller stepping t, t+1, ... finds the next projection ready; any
-// other t is generated on the spot.  A slot is refilled only after the copy
-// that last read it (kProjectionSlots - 1 calls earlier) has completed.
+// Pinned staging of this step's projections and the kernel that moves them
+// into V on the stream.  Once that is queued, the pool starts on V_{t+1} in
+// the next slot of the ring, so that a caller stepping t, t+1, ... finds the
+// next projection ready; any other t is generated on the spot.  A slot is
+// refilled only after the staging kernel that last read it
+// (kProjectionSlots - 1 calls earlier) has completed.
 arc_status upload_projection(arc_ctx* c, int64_t t) {
   const int s = c->V_slot;
   const int next = (s + 1) % arc::kProjectionSlots;

@@ -22,8 +22,9 @@ namespace arc {
 constexpr int kEventsPerStep = 6;
 
 // Pinned host buffers staging V_t, used in turn: a step refills a buffer only
-// once the device has copied it in, so the host can queue this many steps
-// minus one ahead of the device before it waits.
+// once the device has read it (the staging kernel of the step that last used
+// it), so the host can queue this many steps minus one ahead of the device
+// before it waits.
 constexpr int kProjectionSlots = 4;
 
 // Record `why` as the calling thread's last error and return s.
@@ -56,8 +57,8 @@ struct arc_ctx {
   std::vector<int64_t> widths;
   std::map<int64_t, int64_t> v_off;
   int64_t v_floats = 0;
-  // row groups: the vectorisable ones by group size (64, 32, 16 rows), then
-  // the general ones
+  // row groups: the vectorisable ones by group size (64, 32, 16, 8 rows),
+  // then the general ones
   std::vector<arc::RowGroup> groups;
   int64_t nvec_groups = 0;
   std::array<int64_t, 4> vec_count{};  // groups of 64, 32, 16 and 8 rows
