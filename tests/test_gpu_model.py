@@ -56,6 +56,17 @@ def run_model_case(*, d, N, n=0, tensors=None, r=4, K=0, eta=0.1, seed=3, grad_d
             torch.cuda.synchronize(dev)
             if t < dense_steps:
                 oracle.dense_step(h_o, g_o, G_o, grad_np, eta)
+            elif compressor == "randk":
+                if tensors is None:
+                    want = oracle.step_randk(h_o, g_o, grad_np, eta=eta, seed=seed, t=t, n=n, K=K)
+                    oracle.accumulate(G_o, want["idx"], want["agg"], n=n)
+                else:
+                    want = oracle.step_randk(h_o, g_o, grad_np, eta=eta, seed=seed, t=t,
+                                             tensors=tensors)
+                    oracle.accumulate(G_o, want["idx"], want["agg"], tensors=tensors)
+                assert np.array_equal(idx.cpu().numpy(), want["idx"]), f"{label} t={t} idx"
+                compare_float(f"{label} t={t} agg", agg.cpu().numpy().reshape(-1),
+                              want["agg"].reshape(-1))
             elif compressor == "topk":
                 if tensors is None:
                     want = oracle.step_topk(h_o, g_o, grad_np, eta=eta, n=n, K=K)
