@@ -1,8 +1,8 @@
 /* Drives the host-side paths of libarctopk that need no device: status
  * strings, the host projection, configuration checks (every rejection),
  * the create-time planning of valid layouts (single view, buckets, per-tensor
- * views of many widths, the comparison compressors) and the NULL-context
- * paths.  Built against a copy of the library whose host code carries
+ * views of many widths, the comparison compressors, and 300 seeded random
+ * layouts) and the NULL-context paths.  Built against a copy of the library whose host code carries
  * AddressSanitizer; prints "ok" when every check holds.
  *
  * Without a device, arc_create of a valid configuration plans the layout,
@@ -165,6 +165,56 @@ int main(void) {
       c.compressor = ARC_COMP_TOPK; expect_planned(&c, __LINE__);
       c.compressor = ARC_COMP_RANDK; expect_planned(&c, __LINE__);
     }
+  }
+
+  /* seeded random layouts through the planner (single views with buckets,
+   * per-tensor mixes, every compressor) */
+  {
+    uint64_t x = 0x9E3779B97F4A7C15ull;
+#define NEXT() (x = x * 6364136223846793005ull + 1442695040888963407ull, (x >> 33))
+    for (int it = 0; it < 300; ++it) {
+      arc_config c = base();
+      c.N = 1 + (int32_t)(NEXT() % 9);
+      c.r = 1 + (int32_t)(NEXT() % 8);
+      c.compressor = (int32_t)(NEXT() % 3);
+      c.grad_dtype = (int32_t)(NEXT() % 2);
+      arc_tensor t[12];
+      int64_t begin[6], ks[5];
+      if (it % 2 == 0) {
+        const int64_t widths[] = {1, 3, 4, 7, 64, 100, 147, 256, 512, 768, 2048, 4608};
+        const int nt = 1 + (int)(NEXT() % 12);
+        int64_t d = 0;
+        for (int k = 0; k < nt; ++k) {
+          t[k].cols = widths[NEXT() % 12];
+          t[k].rows = 1 + (int64_t)(NEXT() % 700);
+          t[k].K = (int64_t)(NEXT() % (uint64_t)(t[k].rows + 3));
+          d += t[k].rows * t[k].cols;
+        }
+        c.n = 0;
+        c.K = 0;
+        c.d = d;
+        c.tensors = t;
+        c.num_tensors = nt;
+      } else {
+        c.n = 1 + (int64_t)(NEXT() % 5000);
+        c.d = 1 + (int64_t)(NEXT() % 3000000);
+        const int64_t m = (c.d + c.n - 1) / c.n;
+        c.K = (int64_t)(NEXT() % (uint64_t)(m + 2));
+        if (m >= 5 && NEXT() % 2) {
+          const int nb = 1 + (int)(NEXT() % 4);
+          begin[0] = 0;
+          for (int b = 1; b < nb; ++b) begin[b] = begin[b - 1] + 1 + (int64_t)(NEXT() % (uint64_t)(m / nb));
+          begin[nb] = m;
+          for (int b = 0; b < nb; ++b) ks[b] = (int64_t)(NEXT() % 50);
+          c.num_buckets = nb;
+          c.bucket_row_begin = begin;
+          c.bucket_K = ks;
+          c.K = 0;
+        }
+      }
+      expect_planned(&c, __LINE__);
+    }
+#undef NEXT
   }
 
   /* NULL-context paths */
