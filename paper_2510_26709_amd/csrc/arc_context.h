@@ -126,10 +126,14 @@ struct arc_ctx {
     ws.any_radix = 0;
     ws.any_output = 0;
     ws.small = 1;
+    ws.small_rows = 0;
     for (const auto& b : buckets) {
       ws.any_radix |= b.mode == arc::kSelectRadix;
       ws.any_output |= b.mode != arc::kSelectNone;
       ws.small &= b.hi - b.lo <= arc::kSmallBucketRows;
+      if (b.mode == arc::kSelectRadix && b.hi - b.lo > ws.small_rows)
+        ws.small_rows = static_cast<int32_t>(
+            b.hi - b.lo < arc::kSmallBucketRows ? b.hi - b.lo : arc::kSmallBucketRows);
     }
     return ws;
   }

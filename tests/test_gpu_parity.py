@@ -41,7 +41,11 @@ CASES = [
     ("single_worker", dict(d=128 * 640, N=1, n=128, r=4, K=20, steps=2)),
     ("eta_one", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=1.0, steps=2)),
     ("eta_zero", dict(d=256 * 80, N=2, n=256, r=4, K=8, eta=0.0, steps=2)),
-    ("select_multiblock", dict(d=32 * 9000, N=2, n=32, r=4, K=2500, steps=2)),
+    # one workgroup per bucket up to 32,768 rows, the multi-block radix
+    # kernels above that
+    ("select_one_workgroup_9000", dict(d=32 * 9000, N=2, n=32, r=4, K=2500, steps=2)),
+    ("select_one_workgroup_max", dict(d=8 * 32_768, N=2, n=8, r=4, K=3001, steps=2)),
+    ("select_multiblock", dict(d=8 * 32_769, N=2, n=8, r=4, K=3001, steps=2)),
     ("per_worker_N12", dict(d=256 * 300, N=12, n=256, r=4, K=7, steps=2)),
     ("bf16_odd_chunks", dict(d=96 * 700 + 12, N=3, n=96, r=4, K=9, steps=2, grad_dtype="bf16",
                              family=1)),
@@ -192,9 +196,9 @@ def test_parity_buckets():
     run_case(label="buckets", d=d, N=3, n=n, r=4, buckets=(begin, ks), steps=3)
 
 
-# Selections over at most 8192 rows per bucket take the one-workgroup path,
+# Selections over at most 32,768 rows per bucket take the one-workgroup path,
 # larger ones the multi-block radix kernels: both sizes for the tie cases.
-@pytest.mark.parametrize("rows", [400, 40_000])
+@pytest.mark.parametrize("rows", [400, 20_000, 40_000])
 def test_parity_zero_residual_ties_take_lowest_rows(rows):
     d, N, n = 32 * rows, 2, 32
     zero = np.zeros((N, d), F32)
@@ -202,7 +206,7 @@ def test_parity_zero_residual_ties_take_lowest_rows(rows):
     run_case(label=f"zeros_{rows}", d=d, N=N, n=n, K=13, steps=2, grad_fn=lambda t: zero)
 
 
-@pytest.mark.parametrize("rows,K", [(5000, 1234), (70_000, 17_321)])
+@pytest.mark.parametrize("rows,K", [(5000, 1234), (32_768, 9_001), (70_000, 17_321)])
 def test_parity_crafted_ties(rows, K):
     # V = ones (r = 1): Sigma_p = (sum over workers and row of Delta)^2, built
     # from small integers so that many rows tie exactly at the threshold.
@@ -218,6 +222,32 @@ def test_parity_crafted_ties(rows, K):
     log(f"[parity] crafted ties, {rows} rows")
     run_case(label=f"ties_{rows}", d=d, N=N, n=n, r=1, K=K, eta=1.0, steps=1, grad_fn=grad,
              V=np.ones((n, 1), F32))
+
+
+# A bucket of more than 256 blocks x 8192 rows (2,097,152) gives every
+# selection block more than one tile of keys (here 9,984 rows a block: a
+# full tile and a partial one); the ties at the threshold then run across
+# tiles as well as blocks.
+@pytest.mark.parametrize("kind", ["zeros", "ties"])
+def test_parity_multi_tile_selection_blocks(kind):
+    rows, n, N = 2_500_000, 4, 2
+    d = n * rows
+    log(f"[parity] multi-tile selection blocks, {kind}")
+    if kind == "zeros":
+        zero = np.zeros((N, d), F32)
+        run_case(label="zeros_multitile", d=d, N=N, n=n, K=2_400_001, steps=2,
+                 grad_fn=lambda t: zero)
+        return
+    rng = np.random.default_rng(6)
+    vals = rng.integers(0, 4, size=(rows,)).astype(F32)
+
+    def grad(t):
+        g = np.zeros((N, d), F32)
+        g[0, ::n] = vals
+        return g
+
+    run_case(label="ties_multitile", d=d, N=N, n=n, r=1, K=1_000_003, eta=1.0, steps=1,
+             grad_fn=grad, V=np.ones((n, 1), F32))
 
 
 def test_parity_injected_projection():
