@@ -975,7 +975,7 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
                 "compressor=%s mode=%s sketch=%s widths=%zu row_groups=%lld vector_groups=%lld "
                 "(64:%lld 32:%lld 16:%lld 8:%lld rows) workgroup_waves=(%d%s %d%s %d%s %d%s) "
                 "interleaved_groups=%lld general_groups=%lld "
-                "lds_limit=%zu buckets=%zu radix_buckets=%d select_blocks=%zu K_total=%lld "
+                "lds_limit=%zu buckets=%zu radix_buckets=%d select=%s%s K_total=%lld "
                 "payload=%lld",
                 comp, c->tensor_mode ? "tensors" : "single_view", sketch, c->widths.size(),
                 static_cast<long long>(ngroups), static_cast<long long>(c->nvec_groups),
@@ -987,7 +987,9 @@ arc_status arc_describe(const arc_ctx* c, char* buf, int64_t len) {
                 c->vec_occ[3].waves, c->vec_occ[3].one_per_cu ? "/cu" : "", strided,
                 static_cast<long long>(ngroups - c->nvec_groups),
                 c->max_lds_per_block, c->buckets.size(),
-                radix, c->blocks.size(), static_cast<long long>(c->K_total),
+                radix, c->select_ws().small ? "one_workgroup_per_bucket" : "blocks:",
+                c->select_ws().small ? "" : std::to_string(c->blocks.size()).c_str(),
+                static_cast<long long>(c->K_total),
                 static_cast<long long>(c->payload));
   return ARC_OK;
 }

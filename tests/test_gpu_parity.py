@@ -133,6 +133,13 @@ def test_describe_names_the_kernel_path():
         assert "sketch=general" in comp.describe()
     finally:
         comp.close()
+    # one workgroup per bucket up to 32,768 rows, then the multi-block kernels
+    for rows, want in ((32_768, "select=one_workgroup_per_bucket"), (32_769, "select=blocks:5")):
+        comp = arc.Compressor(d=8 * rows, N=1, n=8, K=3, eta=0.1, seed=1)
+        try:
+            assert want in comp.describe(), comp.describe()
+        finally:
+            comp.close()
     # the widest vectorised rows, and one step wider
     for n, want in ((1 << 22, "general_groups=0"), ((1 << 22) + 4, "sketch=general")):
         comp = arc.Compressor(d=n * 2, N=2, n=n, r=4, K=1, eta=0.1, seed=1)
