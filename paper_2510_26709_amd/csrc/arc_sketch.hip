@@ -31,6 +31,9 @@ struct GroupShape {
   static constexpr int kRowF4 = kLanesPerRow + 1;
 };
 constexpr int kTileF4 = 576;  // >= G * (512 / G + 1) for every G
+// Rows of fewer chunks than this keep unshifted windows where the shift onto
+// whole lines would add a chunk (see sketch_rows).
+constexpr uint32_t kShiftMinChunks = 3;
 
 // (row, k) lanes: when G * R <= 64, lane l runs only the chain of row l % G
 // against column (l / G) % R of V, and the R results of a row are collected
@@ -67,7 +70,9 @@ constexpr uint32_t kDropOffset = 0x80000000u;
 // row.  Local row l of the group starts at coordinate elem_off + l*stride*n;
 // n is a multiple of 4 but need not be one of the chunk width, in which case
 // each row's last chunk is partial: its lanes past the row's end load and
-// store nothing, and the chains stop at the row's end.  The three streams are
+// store nothing, and the chains stop at the row's end.  Rows that start off
+// a 128-byte line take chunks shifted onto whole lines (below), with a
+// partial first chunk as well.  The three streams are
 // read through buffer resources that end at the group's last row, so in a
 // group of fewer than G rows (always consecutive rows, stride 1) the missing
 // rows read as zero and are not stored.
@@ -102,22 +107,49 @@ __device__ __forceinline__ void sketch_rows(
       BF16 ? make_buffer(static_cast<const uint16_t*>(grad) + wbase, bytes / 2)
            : make_buffer(static_cast<const float*>(grad) + wbase, bytes);
   V += grp.v_off;
-  // byte offset of this lane's 16 bytes of binary32 in row u*kRPL + sub
+  // Column windows on whole 128-byte lines.  Where every row of the group
+  // starts the same number of bytes past a line of h (one row, or a row
+  // pitch that is a multiple of 128 bytes), chunk c covers the columns
+  // [c*kCW - shift, (c+1)*kCW - shift) rather than [c*kCW, (c+1)*kCW), with
+  // shift the rows' offset from the line in binary32 values (a multiple of
+  // 4, as h is 16-byte aligned): each load instruction then covers whole
+  // lines instead of straddling one more.  The chains still take a row's
+  // columns in ascending order, so the results do not change.  A row can
+  // gain a chunk, which rows of one or two chunks cannot afford.  Stage ms,
+  // 8 binary32 workers whose bases lie 32 bytes apart from the lines, about
+  // 1.2e7 values each, without / with the shift: 512-wide rows (2 chunks)
+  // 0.289 / 0.314, 768 (3) 0.305 / 0.297, 1024 (8, 16-row groups) 0.309 /
+  // 0.264, 1536 (6) 0.312 / 0.289, 2304 (9) 0.330 / 0.311, 4608 (18) 0.351
+  // / 0.322; at 6e7 values each alike.
+  uint32_t shift = 0;
+  if constexpr (G <= 16) {
+    if (rows == 1 || (rstride * n) % 32u == 0u)
+      shift = (uint32_t)(reinterpret_cast<uintptr_t>(h + wbase) & 127u) / 4u;
+    const uint32_t plain = (n + kCW - 1) / kCW;
+    if ((n + shift + kCW - 1) / kCW > plain && plain < kShiftMinChunks) shift = 0;
+  }
+  // byte offset of this lane's 16 bytes of binary32 in row u*kRPL + sub, in
+  // chunk 0 (wrapped below zero for the lanes before a shifted row's start,
+  // whose accesses in chunk 0 are dropped)
   uint32_t off[8];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) off[u] = ((uint32_t)(u * kRPL + sub) * rstride * n + quad * 4) * 4u;
+  for (int u = 0; u < 8; ++u)
+    off[u] = ((uint32_t)(u * kRPL + sub) * rstride * n + quad * 4 - shift) * 4u;
 #pragma unroll
   for (int k = 0; k < R; ++k) s[k] = 0.0f;
   float s_own = 0.0f;  // (row, k) lanes: this lane's chain
 
-  const uint32_t nchunks = (n + kCW - 1) / kCW;
-  // Columns of the last chunk: kCW unless the width is not a multiple of it.
-  const uint32_t tail = n - (nchunks - 1) * kCW;
+  const uint32_t nchunks = (n + shift + kCW - 1) / kCW;
+  // Window positions of the last chunk: kCW unless the shifted width is not
+  // a multiple of it.  Every bound here is a multiple of 4.
+  const uint32_t tail = n + shift - (nchunks - 1) * kCW;
   const bool in_tail = (uint32_t)quad * 4 < tail;
+  const bool in_head = (uint32_t)quad * 4 >= shift;
   // Offset o of this lane's access in chunk c, or kDropOffset (the hardware
-  // drops the access) where the lane is past the end of a partial last chunk.
+  // drops the access) where the lane is before a shifted row's start or
+  // past the end of a partial last chunk.
   auto col_off = [&](uint32_t o, uint32_t c) {
-    return c + 1 < nchunks || in_tail ? o : kDropOffset;
+    return (c > 0 || in_head) && (c + 1 < nchunks || in_tail) ? o : kDropOffset;
   };
   uint2 x_next[8];  // bf16, 64-row groups: this lane's grad of the next chunk
   // Loads of chunk c into xv, hv, gv (off[] at chunk c).  The loop issues
@@ -139,11 +171,14 @@ __device__ __forceinline__ void sketch_rows(
   auto issue_loads = [&](uint32_t c) __attribute__((always_inline)) {
     const bool even = (c & 1) == 0;
     if constexpr (kSliceF4 > 0) {
-      const float4* src = reinterpret_cast<const float4*>(V + (size_t)c * kCW * R);
+      // Chunk c's V rows start at column c*kCW - shift; the positions before
+      // a shifted row's start (no chain reads them) take V's first float4.
+      const float4* src = reinterpret_cast<const float4*>(V);
+      const int first = ((int)(c * kCW) - (int)shift) * R / 4;
 #pragma unroll
       for (int r4 = 0; r4 < kSliceRegs; ++r4)
       {
-        const float4 t = src[slice_at(r4, c)];
+        const float4 t = src[max(first + slice_at(r4, c), 0)];
         vreg[4 * r4] = t.x;
         vreg[4 * r4 + 1] = t.y;
         vreg[4 * r4 + 2] = t.z;
@@ -228,26 +263,20 @@ __device__ __forceinline__ void sketch_rows(
     wave_lds_fence();
     const float* Vc = reinterpret_cast<const float*>(vslice);
     const float4* my_row = tile + (lane & (G - 1)) * kPitch;
-    if constexpr (kSplit) {
-      const float* vk = Vc + ((lane / G) % R) * (kCW + 4);
-      if (c + 1 < nchunks || tail == kCW) {
-#pragma unroll
-        for (int q = 0; q < kLPR; ++q) {
-          const float4 dv = my_row[q];
-          const float4 v4 = *reinterpret_cast<const float4*>(vk + q * 4);
-          s_own = fmaf(dv.x, v4.x, s_own);
-          s_own = fmaf(dv.y, v4.y, s_own);
-          s_own = fmaf(dv.z, v4.z, s_own);
-          s_own = fmaf(dv.w, v4.w, s_own);
-        }
+    // The chains take window positions [4*q0, 4*q1): from a shifted row's
+    // first column in chunk 0, to its last in the last chunk.
+    const int q0 = c == 0 ? (int)shift / 4 : 0;
+    const int q1 = c + 1 < nchunks ? kLPR : (int)tail / 4;
+    auto chain4 = [&](int q) __attribute__((always_inline)) {
+      const float4 dv = my_row[q];
+      if constexpr (kSplit) {
+        const float4 v4 =
+            *reinterpret_cast<const float4*>(Vc + ((lane / G) % R) * (kCW + 4) + q * 4);
+        s_own = fmaf(dv.x, v4.x, s_own);
+        s_own = fmaf(dv.y, v4.y, s_own);
+        s_own = fmaf(dv.z, v4.z, s_own);
+        s_own = fmaf(dv.w, v4.w, s_own);
       } else {
-        const float* rowf = reinterpret_cast<const float*>(my_row);
-        for (uint32_t j = 0; j < tail; ++j) s_own = fmaf(rowf[j], vk[j], s_own);
-      }
-    } else if (c + 1 < nchunks || tail == kCW) {
-#pragma unroll
-      for (int q = 0; q < kLPR; ++q) {
-        const float4 dv = my_row[q];
         const float e4[4] = {dv.x, dv.y, dv.z, dv.w};
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
@@ -260,18 +289,12 @@ __device__ __forceinline__ void sketch_rows(
           }
         }
       }
-    } else {
-      // Partial last chunk: the chains end with the row's last column.
-      const float* rowf = reinterpret_cast<const float*>(my_row);
-      for (uint32_t j = 0; j < tail; ++j) {
-        const float e = rowf[j];
-        if constexpr (NORM) {
-          s[0] = fmaf(e, e, s[0]);
-        } else {
+    };
+    if (q0 == 0 && q1 == kLPR) {
 #pragma unroll
-          for (int k = 0; k < R; ++k) s[k] = fmaf(e, Vc[j * R + k], s[k]);
-        }
-      }
+      for (int q = 0; q < kLPR; ++q) chain4(q);
+    } else {
+      for (int q = q0; q < q1; ++q) chain4(q);
     }
     wave_lds_fence();
   }

@@ -193,6 +193,21 @@ def test_parity_misaligned_pointers_take_the_general_path(n, rows):
     run_case(label=f"misaligned_{n}", d=n * rows, N=3, n=n, r=4, K=11, steps=2, misalign=1)
 
 
+# Pointers 16-byte aligned but 16 to 112 bytes past a 128-byte line, and
+# worker bases further off the lines (d = rows * n + 40): the 8- and 16-row
+# groups shift their column windows onto whole lines, a row's first and last
+# windows partial.
+@pytest.mark.parametrize("n,rows,dtype,mis", [
+    (512, 300, "f32", 4), (512, 300, "f32", 28), (768, 200, "f32", 12),
+    (256, 400, "bf16", 8), (2048, 80, "bf16", 24), (4096, 40, "f32", 16),
+    (1536, 90, "bf16", 16)])
+def test_parity_line_shifted_windows(n, rows, dtype, mis):
+    log(f"[parity] shifted windows n={n} {dtype} misalign={mis}")
+    run_case(label=f"shifted_{n}_{dtype}_{mis}", d=n * rows + 40, N=3, n=n, r=4, K=13,
+             steps=2, grad_dtype=dtype, family=1 if dtype == "bf16" else 0, misalign=mis,
+             check_S=True)
+
+
 def test_parity_buckets():
     # buckets: radix, dense (K >= rows), empty selection, one-row bucket
     n = 64
