@@ -192,7 +192,9 @@ arc_status arc_create(const arc_config *cfg, void *hip_stream, arc_ctx **out);
  * values, by how many rows it streams together), its workgroups each hold
  * just over half of a compute unit's LDS, so that one runs per compute
  * unit: while it runs, another kernel's workgroups that need more than the
- * remaining LDS wait for a compute unit to free up.
+ * remaining LDS wait for a compute unit to free up.  When every bucket has
+ * at most 32,768 rows, the selection runs one 1024-thread workgroup per
+ * bucket holding the bucket's importances in up to 143 KB of LDS.
  */
 arc_status arc_step(arc_ctx *ctx, int64_t t, const void *grad, float *h,
                     float *g, int32_t *out_idx, float *out_agg);
@@ -314,8 +316,9 @@ const char *arc_last_error(void);
 
 /* Write a one-line, NUL-terminated description of how the context runs a
  * step for pointers that take the vectorised path (kernel variants, LDS per
- * block and the device limit, selection blocks) into buf (at most len bytes,
- * truncated).  Host only. */
+ * block and the device limit, the selection's path: one workgroup per
+ * bucket or its number of blocks) into buf (at most len bytes, truncated).
+ * Host only. */
 arc_status arc_describe(const arc_ctx *ctx, char *buf, int64_t len);
 
 /* Enqueue a copy of the last step's importance Sigma ([m] binary32) into the
