@@ -326,8 +326,6 @@ select_write_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
         eq_rank0 >= kleft ? 0 : ((kleft - eq_rank0) < n_eq ? (kleft - eq_rank0) : n_eq);
     const uint32_t n_sel = n_gt + (uint32_t)ties_kept;
     const uint64_t taken_before = (uint64_t)eq_before < kleft ? eq_before : kleft;
-    // The scan's barriers also order this tile's reads of `staged` before
-    // the next tile's writes.
     int64_t pos = bk.out_off + (int64_t)gt_before + (int64_t)taken_before +
                   block_exclusive_scan(n_sel);
     uint64_t rank = eq_rank0;
@@ -349,7 +347,7 @@ select_write_kernel(const float* __restrict__ sigma, SelectWorkspace ws,
     }
     gt_before += tile_both & 0xffffu;
     eq_before += tile_both >> 16;
-    __syncthreads();
+    __syncthreads();  // this tile's reads of `staged` before the next tile's writes
   }
 }
 
