@@ -61,6 +61,25 @@ def test_random_layout_parity(name, kw):
     run_case(label=name, steps=2, seed=7 + len(name), **kw)
 
 
+# Pointers 16-byte aligned but 0 to 112 bytes past a 128-byte line (gradient
+# kept 16-byte aligned for bf16): rows off the lines take the shifted
+# column windows of the 8- and 16-row kernels.
+OFFLINE_CASES = []
+_orng = np.random.default_rng(20262)
+for _k in range(24):
+    _kw = _single_view_case(_orng) if _k % 3 else _tensor_case(_orng)
+    _mis = int(_orng.choice([0, 4, 8, 12, 16, 20, 24, 28]))
+    if _kw["grad_dtype"] == "bf16" and _mis % 8:
+        _mis += 4
+    OFFLINE_CASES.append((f"offline{_k}_{_mis}", dict(_kw, misalign=_mis)))
+
+
+@pytest.mark.parametrize("name,kw", OFFLINE_CASES, ids=[c[0] for c in OFFLINE_CASES])
+def test_random_layout_off_line_pointers(name, kw):
+    log(f"[random] {name}")
+    run_case(label=name, steps=2, seed=5 + len(name), check_S="tensors" not in kw, **kw)
+
+
 from test_gpu_model import run_model_case  # noqa: E402
 
 MODEL_CASES = []
