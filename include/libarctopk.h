@@ -256,9 +256,9 @@ arc_status arc_model_step(arc_ctx *ctx, const arc_model_config *mc, int64_t t,
                           float *opt_m, float *opt_v, int32_t *out_idx, float *out_agg);
 
 /*
- * Allocation-free step, for callers that cannot allocate device memory (code
- * under HIP graph capture, tight serving loops, harnesses that forbid
- * hipMalloc): the same step as arc_create + arc_step (same kernels, same
+ * Allocation-free step, for callers that cannot allocate device memory
+ * (tight serving loops, harnesses that forbid hipMalloc): the same step as
+ * arc_create + arc_step (same kernels, same
  * bits for every output) from a configuration, with no context.  Every
  * device buffer the step needs beyond the caller's grad, h, g, out_idx and
  * out_agg (the kernels' tables, V_t, the per-worker sketch, the importance,
@@ -279,7 +279,9 @@ arc_status arc_model_step(arc_ctx *ctx, const arc_model_config *mc, int64_t t,
  * contents behind: calls on one device that overlap in time (two streams,
  * or two host threads) race and give undefined results; calls in stream
  * order, or on one stream, are safe.  Before refilling its host copy of the
- * tables the call waits until the device has read the previous call's.
+ * tables the call waits until the device has read the previous call's.  As
+ * it copies from host memory and may wait on the device, the call is not
+ * meant for capture into a HIP graph.
  */
 #define ARC_STATIC_SCRATCH_BYTES (64u * 1024u * 1024u)
 arc_status arc_step_static(const arc_config *cfg, void *hip_stream, int64_t t,
