@@ -116,8 +116,9 @@ __device__ __forceinline__ void sketch_rows(
   // lines instead of straddling one more.  The chains still take a row's
   // columns in ascending order, so the results do not change.  A row can
   // gain a chunk, which rows of one or two chunks cannot afford.  Stage ms,
-  // 8 binary32 workers whose bases lie 32 bytes apart from the lines, about
-  // 1.2e7 values each, without / with the shift: 512-wide rows (2 chunks)
+  // 8 binary32 workers of about 1.2e7 values each, d = 8 mod 32 (each
+  // worker's base 32 bytes further past a line than the previous one's),
+  // without / with the shift: 512-wide rows (2 chunks)
   // 0.289 / 0.314, 768 (3) 0.305 / 0.297, 1024 (8, 16-row groups) 0.309 /
   // 0.264, 1536 (6) 0.312 / 0.289, 2304 (9) 0.330 / 0.311, 4608 (18) 0.351
   // / 0.322; at 6e7 values each alike.
